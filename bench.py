@@ -1,0 +1,275 @@
+"""Benchmark of one AsyncLane decode step's hot path on one MI355X.
+
+A step = lane_attn_forward (with compact-refresh rows when the workload has
+them) + lmhead_confidence over the masked positions + select_unmask, on
+seeded synthetic inputs already resident in HBM.  Prints ONE JSON line.
+
+value       (attention FLOPs + LM-head FLOPs) / step time, in TFLOP/s
+roofline    the LM-head kernel (the step's dominant kernel) against HBM:
+            algorithmic bytes per launch / its measured average duration
+cpu_baseline the fp64 oracle on a bounded sample of the same workload,
+            timed on this host's cores
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+WORKLOAD_NAMES = {
+    "tiny": "tiny (4 heads, D 64, P 128, 2 lanes x 32, d 256, V 1024)",
+    "llada": "LLaDA-8B-shaped layer + LM head (32/32 heads, D 128, P 512, 4 lanes x 32 "
+             "linear tree, d 4096, V 126464, 60% masked)",
+    "dream": "Dream-7B-shaped GQA layer + LM head (28/4 heads, D 128, P 1024, 8 lanes x 32, "
+             "d 3584, V 152064, 50% masked)",
+    "long": "long generation, LLaDA shape (P 2048, 16 lanes x 32 depth<=6, 40% masked)",
+    "wide": "wide lane set + compact refresh (P 4096, 32 lanes x 64 depth<=8, 410 refresh "
+            "rows, 30% masked)",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="llada", choices=list(WORKLOAD_NAMES))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-reps", type=int, default=50)
+    return ap.parse_args()
+
+
+def depth_of(parent):
+    out = []
+    for i in range(len(parent)):
+        dd, j = 0, int(parent[i])
+        while j >= 0:
+            dd, j = dd + 1, int(parent[j])
+        out.append(dd)
+    return out
+
+
+def attention_flops(s):
+    """Visible query-key pairs x 4 D (QK^T and PV), per query head."""
+    pairs = sum(s.B * (s.P + s.B * (dd + 1)) for dd in depth_of(s.parent))
+    f = 4.0 * s.Hq * s.D * pairs
+    f += 4.0 * s.Hq * s.D * s.n_ref * s.P
+    return f
+
+
+def lmhead_flops(s):
+    return 2.0 * s.N * s.d * s.V
+
+
+def lmhead_bytes(s):
+    """W once + the scored hidden rows + conf/argmax/lse per row."""
+    return 2.0 * s.V * s.d + 2.0 * s.N * s.d + 12.0 * s.N
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("lmhead.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2606_08411_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(config):
+    """HBM bytes per launch of the LM-head kernel from the committed
+    rocprofv3 counter summary, or None when it is missing or was taken on
+    another version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", f"lmhead_conf_kernel_{config}_pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(s):
+    """The oracle as it stands, on a bounded sample of the workload: every
+    attention head of two query rows per lane, 4 masked rows of the LM head
+    over the whole vocabulary, and the full selection step."""
+    import numpy as np
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(x.get("num_threads", 1)) for x in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    f32 = synth.bf16_bits_to_f32
+    t0 = time.perf_counter()
+    rows = [i * s.B + a for i in range(s.L) for a in (0, s.B - 1)]
+    oracle.attention.lane_attention_rows(f32(s.q), f32(s.k_lane), f32(s.v_lane), f32(s.k_pre),
+                                         f32(s.v_pre), s.parent, s.B, rows)
+    t1 = time.perf_counter()
+    nlm = min(4, s.N)
+    ref = oracle.lmhead.lmhead_confidence_full(f32(s.hidden), s.row_pos[:nlm], f32(s.W),
+                                               s.suppress_eos[:nlm], s.eos_id)
+    t2 = time.perf_counter()
+    conf = np.zeros(s.N)
+    arg = np.zeros(s.N, dtype=np.int64)
+    conf[:nlm], arg[:nlm] = ref["conf"], ref["argmax"]
+    oracle.select.select_unmask(conf, arg, s.row_pos, s.tokens, s.is_masked, s.B, s.role, s.b_len,
+                                s.t_lane, 0, s.tau, s.fallback_k)
+    t3 = time.perf_counter()
+    depth = depth_of(s.parent)
+    f_attn = sum(4.0 * s.D * (s.P + s.B * (depth[r // s.B] + 1)) for r in rows) * s.Hq
+    f_lm = 2.0 * nlm * s.d * s.V
+    # Scale each part to the whole step's work, then to TFLOP/s of the step.
+    t_step = (t1 - t0) * attention_flops(s) / f_attn + (t2 - t1) * lmhead_flops(s) / f_lm + (t3 - t2)
+    return {
+        "value": (attention_flops(s) + lmhead_flops(s)) / t_step / 1e12,
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": f"fp64 oracle: all {s.Hq} heads of {len(rows)} lane query rows, {nlm} of {s.N} "
+                  f"masked LM-head rows over all {s.V} vocab ids, full selection; scaled to one "
+                  f"step ({t3 - t0:.1f} s measured)",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
+              "this build has no multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2606_08411_amd as al
+    import synth
+
+    s = synth.make_step(args.config, args.seed)
+    dev = torch.device("cuda:0")
+
+    def bf(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, kl, vl = bf(s.q), bf(s.k_lane), bf(s.v_lane)
+    kp, vp = bf(s.k_pre), bf(s.v_pre)
+    hidden, W = bf(s.hidden), bf(s.W)
+    row_pos = torch.from_numpy(s.row_pos).to(dev)
+    sup = torch.from_numpy(s.suppress_eos).to(dev)
+    n_ref = s.n_ref
+    ref_args = {}
+    if n_ref:
+        ref_args = dict(refresh_idx=torch.from_numpy(s.refresh_idx).to(dev), q_ref=bf(s.q_ref),
+                        k_ref=bf(s.k_ref), v_ref=bf(s.v_ref))
+    o = torch.empty_like(q)
+    lse = torch.empty((q.shape[0], s.Hq), dtype=torch.float32, device=dev)
+    o_ref = torch.empty_like(ref_args["q_ref"]) if n_ref else None
+    lse_ref = torch.empty((n_ref, s.Hq), dtype=torch.float32, device=dev) if n_ref else None
+    conf = torch.empty(s.N, dtype=torch.float32, device=dev)
+    arg = torch.empty(s.N, dtype=torch.int32, device=dev)
+    lm_lse = torch.empty(s.N, dtype=torch.float32, device=dev)
+    nsteps = args.warmup + args.steps
+    toks = [torch.from_numpy(s.tokens).to(dev) for _ in range(nsteps)]
+    msks = [torch.from_numpy(s.is_masked).to(dev) for _ in range(nsteps)]
+    sel_out = None
+
+    def attn():
+        al.lane_attn_forward(q, kl, vl, kp, vp, s.parent, s.B, o=o, lse=lse, o_ref=o_ref,
+                             lse_ref=lse_ref, **ref_args)
+
+    def lm():
+        al.lmhead_confidence(hidden, W, row_idx=row_pos, suppress_eos=sup, eos_id=s.eos_id,
+                             conf=conf, argmax=arg, lse=lm_lse)
+
+    def select(i):
+        nonlocal sel_out
+        sel_out = al.select_unmask(conf, arg, row_pos, toks[i], msks[i], s.L, s.B, s.role, s.b_len,
+                                   s.t_lane, al.MODE_THRESHOLD, s.tau, s.fallback_k,
+                                   delim_ids=s.delim_ids, eos_id=s.eos_id, rho_min=s.rho_min,
+                                   t_min=s.t_min, out=sel_out)
+
+    def step(i):
+        attn()
+        lm()
+        select(i)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(args.warmup, nsteps):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # Per-call averages (each call enqueues on torch's current stream; the
+    # LM head is a single kernel launch).
+    def timed(fn, reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    reps = args.kernel_reps
+    t_attn = timed(attn, reps)
+    t_lm = timed(lm, reps)
+    t_sel = timed(lambda: select(nsteps - 1), reps)
+
+    f_attn, f_lm = attention_flops(s), lmhead_flops(s)
+    value = (f_attn + f_lm) / (ms_step * 1e-3) / 1e12
+    lm_gbs = lmhead_bytes(s) / (t_lm * 1e-3) / 1e9
+    traffic = measured_traffic(args.config)
+    out = {
+        "metric": "lane-attn + fused LM-head TFLOP/s (MFMA util %), masked positions scored/s",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "seed": args.seed,
+                   "L": s.L, "B": s.B, "P": s.P, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "d": s.d,
+                   "V": s.V, "N_masked": s.N, "n_refresh": n_ref},
+        "mfma_util_pct": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "masked_positions_per_s": round(s.N / (ms_step * 1e-3), 1),
+        "lane_tokens_per_s": round(s.L * s.B / (ms_step * 1e-3), 1),
+        "per_call_ms": {"lane_attn_forward": round(t_attn, 4), "lmhead_confidence": round(t_lm, 4),
+                        "select_unmask": round(t_sel, 4)},
+        "attention_tflops": round(f_attn / (t_attn * 1e-3) / 1e12, 2),
+        "lmhead_tflops": round(f_lm / (t_lm * 1e-3) / 1e12, 2),
+        "roofline": {
+            "kernel": "lmhead_conf_kernel",
+            "bound": "hbm",
+            "achieved": round(lm_gbs, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(lm_gbs / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(s)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

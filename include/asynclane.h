@@ -1,0 +1,232 @@
+/*
+ * asynclane.h -- C ABI of the AsyncLane decode-step hot path on MI355X (gfx950).
+ *
+ * One decode step of AsyncLane (arXiv 2606.08411) evaluates every active lane
+ * of one prefix-sharing group in a single batched model call (Section 3.4,
+ * "Shared-prefix lane batching"), then applies the block-wise sampler's
+ * confidence-based transfer rule inside each lane's valid update region and
+ * reads the lane boundary state that drives forking and advancement
+ * (Section 3.2).  This library provides the data-parallel part of that step
+ * as three calls:
+ *
+ *   lane_attn_forward   shared-prefix lane-batched bidirectional attention
+ *                       (+ compact-refresh row rewrite and refresh rows)
+ *   lmhead_confidence   fused hidden->vocab GEMM + online softmax: per masked
+ *                       position the max probability and its token id,
+ *                       without writing the logits
+ *   select_unmask       per-lane threshold / top-k transfer, write-back,
+ *                       ordered compaction and boundary statistics
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - bf16 tensors are passed as uint16_t bit patterns (al_bf16), row-major,
+ *   innermost index last as written in each shape.
+ * - "dev" pointers are device memory of the current HIP device; "host"
+ *   pointers are read during the call only (their contents are copied into
+ *   kernel arguments before the call returns).
+ * - The caller owns every buffer, including workspaces; the library never
+ *   allocates, frees or keeps a pointer after a call returns.
+ * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *   the call returns before it completes.  Inputs must stay valid until the
+ *   stream reaches that point.
+ * - Return value: AL_OK (0), or a negative AL_ERR_* status.  Argument errors
+ *   are detected before anything is enqueued; AL_ERR_HIP reports a failed
+ *   launch (hipGetLastError after the enqueue).  Nothing is printed and no
+ *   exception crosses the boundary.
+ * - Preconditions that are NOT checked: finite inputs; refresh indices unique
+ *   and in [0, P); row_idx values in [0, n_rows); row_pos strictly ascending
+ *   and in [0, L*B); no overlap between output and input buffers unless a
+ *   parameter is documented as in/out.
+ */
+#ifndef ASYNCLANE_H
+#define ASYNCLANE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t al_bf16;
+
+#define AL_OK 0
+#define AL_ERR_NULL (-1)        /* a required pointer is NULL                     */
+#define AL_ERR_SHAPE (-2)       /* a size or scalar is out of the supported range */
+#define AL_ERR_TREE (-3)        /* parent[i] not in [-1, i)                        */
+#define AL_ERR_WORKSPACE (-4)   /* workspace smaller than the *_workspace_size()   */
+#define AL_ERR_ALIGN (-5)       /* a device pointer is not 16-byte aligned         */
+#define AL_ERR_UNSUPPORTED (-6) /* valid request this build does not implement     */
+#define AL_ERR_HIP (-7)         /* the HIP runtime reported a launch error         */
+
+#define AL_ROLE_GEN 0           /* generate lane: advances the frontier          */
+#define AL_ROLE_REF 1           /* refine lane: polishes a discovered prefix     */
+#define AL_MODE_THRESHOLD 0     /* conf >= tau, optional top-fallback_k          */
+#define AL_MODE_TOPK 1          /* the k_lane[l] most confident positions        */
+
+#define AL_MAX_LANES 64         /* one ancestor set per lane fits a uint64       */
+#define AL_MAX_DELIMS 16
+#define AL_MAX_SELECT_POSITIONS 8192  /* L*B limit of select_unmask              */
+
+/* lane_stats columns (int32 [L][AL_LANE_STATS]) */
+#define AL_STAT_SPLIT 0   /* 0-indexed start of the continuation after the last
+                             delimiter in [0, b_len), 0 if none (eq. split_point) */
+#define AL_STAT_FILLED 1  /* filled (unmasked) positions in [0, b_len)           */
+#define AL_STAT_VALID 2   /* index of the first masked or EOS position, else
+                             b_len (valid prefix length, "Advancement control")   */
+#define AL_STAT_FORK 3    /* 1 iff role = gen, split > 0,
+                             (float)filled >= rho_min * (float)b_len (fp32) and
+                             t_lane >= t_min (eq. fork_condition)                  */
+#define AL_STAT_NSEL 4    /* positions of this lane transferred by this call      */
+#define AL_LANE_STATS 5
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* al_status_string(int status);
+
+/* ------------------------------------------------------------------------
+ * lane_attn_forward -- shared-prefix lane-batched bidirectional attention.
+ *
+ * Defined by Section 3.2 ("Lane-local denoising": a lane is evaluated on its
+ * input given the cached prefix state before the lane) and Section 3.4
+ * ("Shared-prefix lane batching": lanes sharing a prefix state form one
+ * batched call; "Compact cache refresh and reuse": stale prefix rows are
+ * recomputed).  Query row a of lane i and query head h attend, with softmax
+ * scale `scale`, to the key/value rows
+ *     every prefix row 0..P-1
+ *   + every row of the block of each lane j that is i or an ancestor of i
+ *     in the lane tree (parent links), bidirectionally inside the block.
+ * Siblings and descendants are not visible.  K/V head of query head h is
+ * h / (Hq/Hkv).  No bias, soft-cap or positional term is applied (rotary
+ * embedding is the caller's).  Masked positions are ordinary keys.
+ *
+ * With n_refresh > 0 the call first rewrites prefix rows in place,
+ *     k_prefix[refresh_idx[r]] = k_ref[r],  v_prefix[refresh_idx[r]] = v_ref[r],
+ * then computes the lanes over the updated prefix, and computes the
+ * refreshed rows' queries q_ref over all P rows of the updated prefix only.
+ *
+ * q        dev  [L*B][Hq][D]   lane query rows, lane-major (row = i*B + a)
+ * k_lane   dev  [L*B][Hkv][D]  lane block keys (same row order)
+ * v_lane   dev  [L*B][Hkv][D]
+ * k_prefix dev  [P][Hkv][D]    shared cached prefix; in/out when n_refresh>0
+ * v_prefix dev  [P][Hkv][D]
+ * parent   host [L]            parent lane, -1 for a lane attached directly
+ *                              to the prefix; parent[i] must be < i
+ * L        1..AL_MAX_LANES;  B: 16..1024, multiple of 16;  P >= 0
+ * Hq, Hkv  Hq % Hkv == 0, Hq/Hkv <= 16;  D: 64 or 128
+ * scale    softmax scale; <= 0 selects 1/sqrt(D)
+ * refresh_idx dev [n_refresh] int32, unique rows in [0, P); n_refresh >= 0
+ * q_ref    dev  [n_refresh][Hq][D];  k_ref, v_ref dev [n_refresh][Hkv][D]
+ * o_ref    dev  [n_refresh][Hq][D]  out;  lse_ref dev [n_refresh][Hq] fp32 out
+ *          or NULL (all refresh pointers may be NULL when n_refresh == 0)
+ * o        dev  [L*B][Hq][D] out (bf16, round-to-nearest-even)
+ * lse      dev  [L*B][Hq] fp32 out (natural-log sum of exp of scaled
+ *          scores), or NULL
+ * workspace dev, >= lane_attn_workspace_size(...) bytes (may be NULL when
+ *          that size is 0); contents need not be initialised
+ * ------------------------------------------------------------------------ */
+size_t lane_attn_workspace_size(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh);
+
+int lane_attn_forward(const al_bf16* q, const al_bf16* k_lane, const al_bf16* v_lane,
+                      al_bf16* k_prefix, al_bf16* v_prefix,
+                      const int32_t* parent, int L, int B, int P,
+                      int Hq, int Hkv, int D, float scale,
+                      const int32_t* refresh_idx, int n_refresh,
+                      const al_bf16* q_ref, const al_bf16* k_ref, const al_bf16* v_ref,
+                      al_bf16* o_ref, float* lse_ref,
+                      al_bf16* o, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * lmhead_confidence -- LM-head GEMM fused with an online softmax.
+ *
+ * Defined by Section 3.2 ("Lane-local denoising"): a lane's outputs feed the
+ * block-wise sampler's confidence-based transfer rule, whose confidence is
+ * the probability of the most likely token; refine lanes suppress EOS.  For
+ * n in [0, N), with r = row_idx[n] (or n when row_idx is NULL):
+ *     z[v]     = sum_k hidden[r][k] * W[v][k]          (fp32 accumulation)
+ *     C        = [0, V) minus eos_id if suppress_eos[n] != 0
+ *     argmax[n]= smallest v in C with z[v] = max_C z
+ *     lse[n]   = log sum_{v in C} exp(z[v])   (natural log)
+ *     conf[n]  = exp(max_C z - lse[n])
+ * The logits are never written to memory.  Results are bitwise
+ * reproducible from call to call (fixed reduction order, no float atomics).
+ *
+ * hidden   dev [n_rows][d]        bf16 hidden states
+ * row_idx  dev [N] int32 or NULL  rows of `hidden` to score (masked positions)
+ * N        0..n_rows (N == 0 enqueues nothing)
+ * W        dev [V][d]             bf16 LM-head weight (nn.Linear layout)
+ * d        multiple of 8, 8..65536;  V: 1..2^30
+ * suppress_eos dev [N] uint8 or NULL (NULL = no row suppresses EOS)
+ * eos_id   in [-1, V); -1 = no EOS id
+ * conf, argmax  dev [N] fp32 / int32 out;  lse dev [N] fp32 out or NULL
+ * workspace dev, >= lmhead_confidence_workspace_size(N, d, V) bytes.  Its
+ *          first 64 KiB hold arrival counters and nothing else, for every
+ *          shape: they must be zero before the first call that uses the
+ *          workspace (e.g. allocate it zero-filled) and every completed call
+ *          leaves them zero again, so one workspace serves calls of any
+ *          shape in sequence.  The rest is scratch.  Calls that share a
+ *          workspace must not run concurrently.  AL_ERR_UNSUPPORTED when the
+ *          counters of a shape would not fit (N beyond ~500k rows).
+ * ------------------------------------------------------------------------ */
+size_t lmhead_confidence_workspace_size(int N, int d, int V);
+
+int lmhead_confidence(const al_bf16* hidden, int n_rows,
+                      const int32_t* row_idx, int N,
+                      const al_bf16* W, int d, int V,
+                      const uint8_t* suppress_eos, int eos_id,
+                      float* conf, int32_t* argmax, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * select_unmask -- per-lane transfer, write-back and boundary statistics.
+ *
+ * Defined by Section 3.2: the transfer rule is applied to each lane's valid
+ * update region [0, b_len[l]) (refine lanes: the discovered prefix); the
+ * transferred positions take their argmax token and are written back; then
+ * the lane's split point (eq. split_point, ValidBoundary taken as true),
+ * fill ratio and step condition (eq. fork_condition) and valid prefix length
+ * ("Advancement control") are computed on the updated state.
+ *
+ * Row n describes flat position row_pos[n] = lane*B + i.  A row is a
+ * candidate of lane l = row_pos[n]/B when i < b_len[l] and the position is
+ * masked.  Order "most confident first": conf descending, then position
+ * ascending.  THRESHOLD mode selects every candidate with conf >= tau (fp32
+ * compare); a lane with none selects its fallback_k most confident
+ * candidates when fallback_k > 0.  TOPK mode selects the min(k_lane[l],
+ * #candidates) most confident candidates of each lane.
+ *
+ * conf, argmax  dev [N] fp32 / int32 (from lmhead_confidence)
+ * row_pos  dev [N] int32, strictly ascending in [0, L*B)
+ * N        0..L*B
+ * tokens   dev [L*B] int32 in/out;  is_masked dev [L*B] uint8 in/out
+ * L        1..AL_MAX_LANES;  B >= 1;  L*B <= AL_MAX_SELECT_POSITIONS
+ * role     host [L] uint8 AL_ROLE_*;  b_len host [L] in [0, B] or NULL (= B);
+ * t_lane   host [L] local denoising steps or NULL (= 0)
+ * mode     AL_MODE_THRESHOLD or AL_MODE_TOPK;  tau fp32 (not NaN)
+ * fallback_k >= 0;  k_lane host [L] >= 0 (required in TOPK mode, else unused)
+ * delim_ids host [n_delim] token ids, 0 <= n_delim <= AL_MAX_DELIMS
+ * eos_id   token id ending the valid prefix (-1 = none)
+ * rho_min, t_min  fork condition parameters
+ * unmask_flag dev [N] uint8 out: 1 iff row n was transferred
+ * unmasked_pos dev [N] int32 out: transferred positions, ascending
+ * still_masked_pos dev [N] int32 out: positions of rows still masked,
+ *          ascending (the next step's row list)
+ * counts   dev [2] int32 out: {#unmasked_pos, #still_masked_pos}
+ * lane_stats dev [L][AL_LANE_STATS] int32 out
+ * delim_flag dev [L*B] uint8 out or NULL: 1 iff the position is < b_len of
+ *          its lane, filled and holds a delimiter id
+ * ------------------------------------------------------------------------ */
+int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_pos, int N,
+                  int32_t* tokens, uint8_t* is_masked, int L, int B,
+                  const uint8_t* role, const int32_t* b_len, const int32_t* t_lane,
+                  int mode, float tau, int fallback_k, const int32_t* k_lane,
+                  const int32_t* delim_ids, int n_delim, int eos_id,
+                  float rho_min, int t_min,
+                  uint8_t* unmask_flag, int32_t* unmasked_pos, int32_t* still_masked_pos,
+                  int32_t* counts, int32_t* lane_stats, uint8_t* delim_flag,
+                  void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ASYNCLANE_H */

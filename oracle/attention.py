@@ -181,3 +181,30 @@ def decode_attention(q, k_lane, v_lane, k_pre, v_pre, parent, B,
     if refresh_idx is not None and len(refresh_idx):
         out["o_ref"], out["lse_ref"] = refresh_attention(q_ref, k_pre, v_pre, scale)
     return out
+
+
+def lane_attention_rows(q, k_lane, v_lane, k_pre, v_pre, parent, B, rows, heads=None,
+                        scale=None):
+    """Outputs of selected query rows only, computed one row at a time on the
+    row's own visible key set (for spot checks at full size).
+    Returns (O [len(rows)][len(heads)][D], LSE [len(rows)][len(heads)])."""
+    LB, Hq, D = q.shape
+    Hkv = k_lane.shape[1]
+    g = Hq // Hkv
+    heads = list(range(Hq)) if heads is None else list(heads)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    anc = lane_ancestors(parent)
+    O = np.zeros((len(rows), len(heads), D))
+    LSE = np.zeros((len(rows), len(heads)))
+    for a, t in enumerate(rows):
+        i = int(t) // B
+        blocks = anc[i] + [i]
+        for b, h in enumerate(heads):
+            kv = h // g
+            kc = np.concatenate([_f64(k_pre[:, kv])] + [_f64(k_lane[j * B:(j + 1) * B, kv]) for j in blocks])
+            vc = np.concatenate([_f64(v_pre[:, kv])] + [_f64(v_lane[j * B:(j + 1) * B, kv]) for j in blocks])
+            o, lse = softmax_attend(_f64(q[t, h])[None, :], kc, vc, scale)
+            O[a, b] = o[0]
+            LSE[a, b] = lse[0]
+    return O, LSE

@@ -1,0 +1,28 @@
+"""AsyncLane decode-step hot path on MI355X (gfx950).
+
+Three calls, backed by hand-written HIP kernels in libasynclane.so:
+
+* ``lane_attn_forward``  shared-prefix lane-batched bidirectional attention
+  over a lane tree, with compact-refresh prefix rows (paper Sections 3.2, 3.4)
+* ``lmhead_confidence``  fused LM-head GEMM + online softmax: per masked
+  position the max probability and its token, logits never stored
+* ``select_unmask``      per-lane threshold / top-k transfer, write-back and
+  lane boundary statistics (eq. split_point, eq. fork_condition)
+
+The functions are thin ctypes wrappers (see ``_lib``); they raise when the
+library has not been built (``python -m paper_2606_08411_amd.build``).
+"""
+from ._lib import (  # noqa: F401
+    AsyncLaneError,
+    LANE_STATS,
+    MODE_THRESHOLD,
+    MODE_TOPK,
+    ROLE_GEN,
+    ROLE_REF,
+    lane_attn_forward,
+    lane_attn_workspace_size,
+    library,
+    lmhead_confidence,
+    lmhead_confidence_workspace_size,
+    select_unmask,
+)

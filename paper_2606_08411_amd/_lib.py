@@ -1,0 +1,245 @@
+"""ctypes binding of libasynclane.so (the C ABI in include/asynclane.h).
+
+Argument marshalling only: every step of the decode-step hot path runs in the
+library's HIP kernels.  PyTorch supplies device memory and the current HIP
+stream.  There is no fallback: when the library is missing or a call fails,
+an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libasynclane.so")
+
+AL_OK = 0
+STATUS = {0: "AL_OK", -1: "AL_ERR_NULL", -2: "AL_ERR_SHAPE", -3: "AL_ERR_TREE",
+          -4: "AL_ERR_WORKSPACE", -5: "AL_ERR_ALIGN", -6: "AL_ERR_UNSUPPORTED",
+          -7: "AL_ERR_HIP"}
+ROLE_GEN, ROLE_REF = 0, 1
+MODE_THRESHOLD, MODE_TOPK = 0, 1
+LANE_STATS = 5
+MAX_SELECT_POSITIONS = 8192
+
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+_f = ctypes.c_float
+_sz = ctypes.c_size_t
+
+_SIGNATURES = {
+    "al_status_string": (ctypes.c_char_p, [_i]),
+    "lane_attn_workspace_size": (_sz, [_i] * 7),
+    "lane_attn_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f,
+                               _vp, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "lmhead_confidence_workspace_size": (_sz, [_i, _i, _i]),
+    "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
+                               _sz, _vp]),
+    "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
+                           _vp, _vp, _i, _i, _f, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+}
+
+_lib = None
+_lock = threading.Lock()
+
+
+class AsyncLaneError(RuntimeError):
+    pass
+
+
+def library() -> ctypes.CDLL:
+    """Load libasynclane.so (raises when it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise AsyncLaneError(
+                    f"{LIB_PATH} is missing: build it with "
+                    "`python -m paper_2606_08411_amd.build` (hipcc, gfx950)")
+            lib = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in _SIGNATURES.items():
+                fn = getattr(lib, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = lib
+    return _lib
+
+
+def _check(status: int, what: str):
+    if status != AL_OK:
+        msg = library().al_status_string(status).decode()
+        raise AsyncLaneError(f"{what} failed: {STATUS.get(status, status)} ({msg})")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise AsyncLaneError("device tensor expected")
+    if not t.is_contiguous():
+        raise AsyncLaneError("contiguous tensor expected")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _host_i32(x, n, name):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+    if a.shape != (n,):
+        raise AsyncLaneError(f"{name}: expected {n} entries")
+    return a
+
+
+def _host_u8(x, n, name):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.uint8))
+    if a.shape != (n,):
+        raise AsyncLaneError(f"{name}: expected {n} entries")
+    return a
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ------------------------------------------------------------ workspaces
+_ws_cache: dict = {}
+
+
+def _workspace(kind: str, nbytes: int, device, zeroed: bool):
+    """Device workspace cached per (kind, device); grown on demand.  The
+    LM-head workspace is zero-filled once: the library leaves its arrival
+    counters at zero after every call."""
+    if nbytes == 0:
+        return None, 0
+    key = (kind, str(device))
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < nbytes:
+        alloc = torch.zeros if zeroed else torch.empty
+        buf = alloc(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
+    return buf, buf.numel()
+
+
+# ------------------------------------------------------------ entry points
+def lane_attn_workspace_size(L, B, P, Hq, Hkv, D, n_refresh=0) -> int:
+    return int(library().lane_attn_workspace_size(L, B, P, Hq, Hkv, D, n_refresh))
+
+
+def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.0,
+                      refresh_idx=None, q_ref=None, k_ref=None, v_ref=None,
+                      o=None, lse=None, o_ref=None, lse_ref=None, want_lse=True,
+                      workspace=None):
+    """Shared-prefix lane-batched attention (+ compact-refresh rows).
+
+    q [L*B][Hq][D], k_lane/v_lane [L*B][Hkv][D], k_prefix/v_prefix
+    [P][Hkv][D] are bf16 device tensors; parent is a host sequence of L ints.
+    k_prefix / v_prefix are updated in place when refresh rows are given.
+    Returns (o, lse, o_ref, lse_ref)."""
+    lib = library()
+    LB, Hq, D = q.shape
+    Hkv = k_lane.shape[1]
+    P = k_prefix.shape[0]
+    L = len(parent)
+    par = _host_i32(parent, L, "parent")
+    n_ref = 0 if refresh_idx is None else int(refresh_idx.shape[0])
+    dev = q.device
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((LB, Hq), dtype=torch.float32, device=dev)
+    if n_ref:
+        if o_ref is None:
+            o_ref = torch.empty_like(q_ref)
+        if lse_ref is None and want_lse:
+            lse_ref = torch.empty((n_ref, Hq), dtype=torch.float32, device=dev)
+    need = int(lib.lane_attn_workspace_size(L, B, P, Hq, Hkv, D, n_ref))
+    if workspace is None:
+        ws, ws_bytes = _workspace("attn", need, dev, zeroed=False)
+    else:
+        ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
+    st = lib.lane_attn_forward(
+        _ptr(q), _ptr(k_lane), _ptr(v_lane), _ptr(k_prefix), _ptr(v_prefix), _np_ptr(par),
+        L, B, P, Hq, Hkv, D, float(scale),
+        _ptr(refresh_idx) if n_ref else None, n_ref,
+        _ptr(q_ref) if n_ref else None, _ptr(k_ref) if n_ref else None,
+        _ptr(v_ref) if n_ref else None, _ptr(o_ref) if n_ref else None,
+        _ptr(lse_ref) if n_ref else None, _ptr(o), _ptr(lse), _ptr(ws), ws_bytes, _stream())
+    _check(st, "lane_attn_forward")
+    return o, lse, o_ref, lse_ref
+
+
+def lmhead_confidence_workspace_size(N, d, V) -> int:
+    return int(library().lmhead_confidence_workspace_size(N, d, V))
+
+
+def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
+                      conf=None, argmax=None, lse=None, want_lse=True, workspace=None):
+    """Per scored row: max softmax probability, its token id and the
+    log-sum-exp over the vocabulary (EOS excluded for suppressed rows).
+    hidden [n_rows][d] and W [V][d] are bf16 device tensors; row_idx is an
+    int32 device tensor (None = every row).  Returns (conf, argmax, lse)."""
+    lib = library()
+    n_rows, d = hidden.shape
+    V = W.shape[0]
+    N = n_rows if row_idx is None else int(row_idx.shape[0])
+    dev = hidden.device
+    if conf is None:
+        conf = torch.empty(N, dtype=torch.float32, device=dev)
+    if argmax is None:
+        argmax = torch.empty(N, dtype=torch.int32, device=dev)
+    if lse is None and want_lse:
+        lse = torch.empty(N, dtype=torch.float32, device=dev)
+    if N == 0:
+        return conf, argmax, lse
+    need = int(lib.lmhead_confidence_workspace_size(N, d, V))
+    if workspace is None:
+        ws, ws_bytes = _workspace("lmhead", need, dev, zeroed=True)
+    else:
+        ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
+    st = lib.lmhead_confidence(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
+                               _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
+                               _ptr(lse), _ptr(ws), ws_bytes, _stream())
+    _check(st, "lmhead_confidence")
+    return conf, argmax, lse
+
+
+def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=None,
+                  t_lane=None, mode=MODE_THRESHOLD, tau=0.9, fallback_k=0, k_lane=None,
+                  delim_ids=(0, 1), eos_id=2, rho_min=0.5, t_min=2, with_delim_flag=True,
+                  out=None):
+    """Per-lane transfer + write-back (tokens / is_masked updated in place),
+    ordered compaction and lane statistics.  Returns a dict of device
+    tensors: unmask_flag, unmasked_pos, still_masked_pos, counts,
+    lane_stats, delim_flag."""
+    lib = library()
+    N = int(row_pos.shape[0])
+    dev = tokens.device
+    role_h = _host_u8(role, L, "role")
+    b_len_h = None if b_len is None else _host_i32(b_len, L, "b_len")
+    t_lane_h = None if t_lane is None else _host_i32(t_lane, L, "t_lane")
+    k_lane_h = None if k_lane is None else _host_i32(k_lane, L, "k_lane")
+    delim_h = np.ascontiguousarray(np.asarray(delim_ids, dtype=np.int32))
+    if out is None:
+        out = dict(
+            unmask_flag=torch.empty(max(N, 1), dtype=torch.uint8, device=dev),
+            unmasked_pos=torch.empty(max(N, 1), dtype=torch.int32, device=dev),
+            still_masked_pos=torch.empty(max(N, 1), dtype=torch.int32, device=dev),
+            counts=torch.empty(2, dtype=torch.int32, device=dev),
+            lane_stats=torch.empty((L, LANE_STATS), dtype=torch.int32, device=dev),
+            delim_flag=torch.empty(L * B, dtype=torch.uint8, device=dev) if with_delim_flag else None)
+    st = lib.select_unmask(
+        _ptr(conf) if N else None, _ptr(argmax) if N else None, _ptr(row_pos) if N else None, N,
+        _ptr(tokens), _ptr(is_masked), L, B, _np_ptr(role_h), _np_ptr(b_len_h), _np_ptr(t_lane_h),
+        int(mode), float(tau), int(fallback_k), _np_ptr(k_lane_h),
+        _np_ptr(delim_h) if len(delim_h) else None, len(delim_h), int(eos_id), float(rho_min),
+        int(t_min), _ptr(out["unmask_flag"]), _ptr(out["unmasked_pos"]),
+        _ptr(out["still_masked_pos"]), _ptr(out["counts"]), _ptr(out["lane_stats"]),
+        _ptr(out["delim_flag"]), _stream())
+    _check(st, "select_unmask")
+    return out

@@ -1,0 +1,170 @@
+// C ABI entry points: argument validation, lane-tree preprocessing and
+// launches on the caller's stream.  Every check runs before anything is
+// enqueued; nothing here allocates, prints or throws.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/asynclane.h"
+#include "launch.h"
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? AL_OK : AL_ERR_HIP; }
+
+// Ancestor-or-self sets of the lane tree: bit j of vis[i] is set when lane j
+// is lane i or one of its ancestors (parent[i] < i, so one forward pass).
+int lane_visibility(const int32_t* parent, int L, unsigned long long* vis) {
+  for (int i = 0; i < L; ++i) {
+    const int pi = parent[i];
+    if (pi < -1 || pi >= i) return AL_ERR_TREE;
+    vis[i] = (1ull << i) | (pi >= 0 ? vis[pi] : 0ull);
+  }
+  return AL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* al_status_string(int status) {
+  switch (status) {
+    case AL_OK: return "ok";
+    case AL_ERR_NULL: return "required pointer is null";
+    case AL_ERR_SHAPE: return "size or scalar out of the supported range";
+    case AL_ERR_TREE: return "lane tree invalid: parent[i] must be in [-1, i)";
+    case AL_ERR_WORKSPACE: return "workspace too small";
+    case AL_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case AL_ERR_UNSUPPORTED: return "unsupported configuration";
+    case AL_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+static bool attn_shape_ok(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
+  if (L < 1 || L > AL_MAX_LANES) return false;
+  if (B < 16 || B > 1024 || B % 16 != 0) return false;
+  if (P < 0 || n_refresh < 0 || n_refresh > P) return false;
+  if (Hkv < 1 || Hq < Hkv || Hq % Hkv != 0 || Hq / Hkv > 16) return false;
+  if (D != 64 && D != 128) return false;
+  if ((long long)L * B * Hq * D >= (1ll << 31) || (long long)P * Hkv * D >= (1ll << 31)) return false;
+  return true;
+}
+
+size_t lane_attn_workspace_size(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
+  if (!attn_shape_ok(L, B, P, Hq, Hkv, D, n_refresh)) return 0;
+  return al::attn_plan(L, B, P, Hq, Hkv, D, n_refresh).total;
+}
+
+int lane_attn_forward(const al_bf16* q, const al_bf16* k_lane, const al_bf16* v_lane,
+                      al_bf16* k_prefix, al_bf16* v_prefix, const int32_t* parent, int L, int B,
+                      int P, int Hq, int Hkv, int D, float scale, const int32_t* refresh_idx,
+                      int n_refresh, const al_bf16* q_ref, const al_bf16* k_ref,
+                      const al_bf16* v_ref, al_bf16* o_ref, float* lse_ref, al_bf16* o, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  if (!q || !k_lane || !v_lane || !parent || !o) return AL_ERR_NULL;
+  if (P > 0 && (!k_prefix || !v_prefix)) return AL_ERR_NULL;
+  if (n_refresh > 0 && (!refresh_idx || !q_ref || !k_ref || !v_ref || !o_ref)) return AL_ERR_NULL;
+  if (!attn_shape_ok(L, B, P, Hq, Hkv, D, n_refresh)) return AL_ERR_SHAPE;
+  if (isnan(scale) || isinf(scale)) return AL_ERR_SHAPE;
+  if (!aligned16(q) || !aligned16(k_lane) || !aligned16(v_lane) || !aligned16(o) ||
+      (P > 0 && (!aligned16(k_prefix) || !aligned16(v_prefix))) || (lse && !aligned4(lse)))
+    return AL_ERR_ALIGN;
+  if (n_refresh > 0 && (!aligned16(q_ref) || !aligned16(k_ref) || !aligned16(v_ref) ||
+                        !aligned16(o_ref) || !aligned4(refresh_idx) || (lse_ref && !aligned4(lse_ref))))
+    return AL_ERR_ALIGN;
+  unsigned long long vis[AL_MAX_LANES];
+  const int tree = lane_visibility(parent, L, vis);
+  if (tree != AL_OK) return tree;
+  const al::AttnPlan plan = al::attn_plan(L, B, P, Hq, Hkv, D, n_refresh);
+  if (plan.total > 0) {
+    if (!workspace) return AL_ERR_NULL;
+    if (workspace_bytes < plan.total) return AL_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return AL_ERR_ALIGN;
+  }
+  const float sc = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
+  return hip_status(al::launch_lane_attention(
+      q, k_lane, v_lane, k_prefix, v_prefix, vis, L, B, P, Hq, Hkv, D, sc, refresh_idx, n_refresh,
+      q_ref, k_ref, v_ref, o_ref, lse_ref, o, lse, workspace, static_cast<hipStream_t>(stream)));
+}
+
+static bool lm_shape_ok(int N, int d, int V) {
+  return N >= 0 && d >= 8 && d <= 65536 && d % 8 == 0 && V >= 1 && V <= (1 << 30);
+}
+
+size_t lmhead_confidence_workspace_size(int N, int d, int V) {
+  if (!lm_shape_ok(N, d, V)) return 0;
+  return al::lmhead_workspace_bytes(N, d, V);
+}
+
+int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
+                      const al_bf16* W, int d, int V, const uint8_t* suppress_eos, int eos_id,
+                      float* conf, int32_t* argmax, float* lse, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  if (!lm_shape_ok(N, d, V) || n_rows < 0 || N > n_rows) return AL_ERR_SHAPE;
+  if (eos_id < -1 || eos_id >= V) return AL_ERR_SHAPE;
+  if (N == 0) return AL_OK;
+  if (!al::lmhead_counters_fit(N, V)) return AL_ERR_UNSUPPORTED;
+  if (!hidden || !W || !conf || !argmax) return AL_ERR_NULL;
+  if (!aligned16(hidden) || !aligned16(W) || !aligned4(conf) || !aligned4(argmax) ||
+      (row_idx && !aligned4(row_idx)) || (lse && !aligned4(lse)))
+    return AL_ERR_ALIGN;
+  const size_t need = al::lmhead_workspace_bytes(N, d, V);
+  if (!workspace) return AL_ERR_NULL;
+  if (workspace_bytes < need) return AL_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return AL_ERR_ALIGN;
+  return hip_status(al::launch_lmhead(hidden, row_idx, N, W, d, V, suppress_eos, eos_id, conf,
+                                      argmax, lse, workspace, static_cast<hipStream_t>(stream)));
+}
+
+int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_pos, int N,
+                  int32_t* tokens, uint8_t* is_masked, int L, int B, const uint8_t* role,
+                  const int32_t* b_len, const int32_t* t_lane, int mode, float tau, int fallback_k,
+                  const int32_t* k_lane, const int32_t* delim_ids, int n_delim, int eos_id,
+                  float rho_min, int t_min, uint8_t* unmask_flag, int32_t* unmasked_pos,
+                  int32_t* still_masked_pos, int32_t* counts, int32_t* lane_stats,
+                  uint8_t* delim_flag, void* stream) {
+  if (L < 1 || L > AL_MAX_LANES || B < 1 || (long long)L * B > al::kSelMaxPositions)
+    return AL_ERR_SHAPE;
+  if (N < 0 || N > L * B) return AL_ERR_SHAPE;
+  if (mode != AL_MODE_THRESHOLD && mode != AL_MODE_TOPK) return AL_ERR_SHAPE;
+  if (isnan(tau) || isnan(rho_min) || fallback_k < 0 || n_delim < 0 || n_delim > AL_MAX_DELIMS)
+    return AL_ERR_SHAPE;
+  if (!tokens || !is_masked || !role || !counts || !lane_stats) return AL_ERR_NULL;
+  if (n_delim > 0 && !delim_ids) return AL_ERR_NULL;
+  if (mode == AL_MODE_TOPK && !k_lane) return AL_ERR_NULL;
+  if (N > 0 && (!conf || !argmax || !row_pos || !unmask_flag || !unmasked_pos || !still_masked_pos))
+    return AL_ERR_NULL;
+  if (!aligned4(tokens) || !aligned4(counts) || !aligned4(lane_stats) ||
+      (N > 0 && (!aligned4(conf) || !aligned4(argmax) || !aligned4(row_pos) ||
+                 !aligned4(unmasked_pos) || !aligned4(still_masked_pos))))
+    return AL_ERR_ALIGN;
+  al::SelHost h{};
+  h.L = L;
+  h.B = B;
+  h.N = N;
+  h.mode = mode;
+  h.tau = tau;
+  h.fallback_k = fallback_k;
+  h.eos_id = eos_id;
+  h.rho_min = rho_min;
+  h.t_min = t_min;
+  h.n_delim = n_delim;
+  for (int j = 0; j < n_delim; ++j) h.delim[j] = delim_ids[j];
+  for (int i = 0; i < L; ++i) {
+    if (role[i] != AL_ROLE_GEN && role[i] != AL_ROLE_REF) return AL_ERR_SHAPE;
+    h.role[i] = role[i];
+    h.b_len[i] = b_len ? b_len[i] : B;
+    if (h.b_len[i] < 0 || h.b_len[i] > B) return AL_ERR_SHAPE;
+    h.t_lane[i] = t_lane ? t_lane[i] : 0;
+    h.k_lane[i] = (mode == AL_MODE_TOPK) ? k_lane[i] : 0;
+    if (h.k_lane[i] < 0) return AL_ERR_SHAPE;
+  }
+  return hip_status(al::launch_select(h, conf, argmax, row_pos, tokens, is_masked, unmask_flag,
+                                      unmasked_pos, still_masked_pos, counts, lane_stats,
+                                      delim_flag, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

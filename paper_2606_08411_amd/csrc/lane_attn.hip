@@ -1,0 +1,456 @@
+// Shared-prefix lane-batched bidirectional attention for gfx950.
+//
+// Paper Section 3.2 ("Lane-local denoising") and Section 3.4 ("Shared-prefix
+// lane batching", "Compact cache refresh and reuse"): every active lane of a
+// prefix-sharing group is evaluated in one batched call; lane i's B query
+// rows see the shared cached prefix, the blocks of its ancestors in the lane
+// tree and, bidirectionally, its own block.
+//
+// Kernel layout.  A workgroup of 4 wavefronts serves one K/V head and four
+// query tiles (32 query rows of one lane and one query head each; for
+// grouped-query attention the Hq/Hkv heads of a lane are adjacent tiles).
+// Key tiles of 64 rows are staged once per workgroup in LDS -- K row-major,
+// V transposed -- and consumed by every wavefront whose lane sees them, so a
+// prefix tile read from HBM serves all lanes of the workgroup.  Both
+// products run transposed on the 32x32x16 bf16 MFMA:
+//     S^T = K Q^T      (lane l owns query row l%32, half of the keys)
+//     O^T = V^T P^T    (lane l owns query row l%32, a quarter of D)
+// so the running max / sum of the online softmax and the rescale of O stay
+// inside a lane pair (l, l^32) and need no cross-lane broadcast.  The key
+// order inside each 16-key MFMA step is permuted identically on both
+// operands to match the S^T accumulator layout (a contraction is invariant
+// under a common permutation of its summed index).
+//
+// Short grids (few heads x few lanes) split the key tiles over blockIdx.z;
+// the splits' unnormalised partials are combined by attn_merge_kernel.
+#include <math.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace al {
+
+constexpr int AT_WAVES = 4;
+constexpr int AT_THREADS = AT_WAVES * kWave;
+constexpr int AT_KT = 64;  // keys per staged tile
+constexpr int AT_MAX_LANES = 64;
+constexpr float AT_LN2 = 0.6931471805599453f;
+
+struct AttnParams {
+  const uint16_t* q;       // [n_rows][Hq][D]
+  const uint16_t* k_lane;  // [n_key_lanes*B_keys][Hkv][D] (lane mode)
+  const uint16_t* v_lane;
+  const uint16_t* k_pre;   // [P][Hkv][D]
+  const uint16_t* v_pre;
+  uint16_t* o;             // [n_rows][Hq][D]
+  float* lse;              // [n_rows][Hq] or null
+  float* part_o;           // [n_split][n_rows][Hq][D] when n_split > 1
+  float* part_ml;          // [n_split][n_rows][Hq][2]
+  int n_rows, rows_per_lane, tiles_per_lane, q_tiles_kv;
+  int P, Hq, Hkv, g;
+  int B_keys, n_key_lanes, lane_key_tiles, n_pre_tiles, total_key_tiles, n_split;
+  float scale_log2;
+  unsigned long long vis[AT_MAX_LANES];  // bit j: lane block j visible to lane i
+};
+
+// Position of key kk (within a 64-key tile) in the transposed V tile: inside
+// each 16-key MFMA step, lane half h reads the 8 contiguous positions
+// [8h, 8h+8), which must hold the keys {4h..4h+3, 8+4h..8+4h+3} that the
+// S^T accumulator gives lane half h.
+__device__ __forceinline__ int vt_pos4(int k4) {  // k4 = kk / 4, returns pos of 4*k4
+  const int q = k4 & 3;
+  return 16 * (k4 >> 2) + 8 * (q & 1) + 4 * (q >> 1);
+}
+
+template <int D>
+__global__ __launch_bounds__(AT_THREADS) void lane_attn_kernel(AttnParams p) {
+  constexpr int KS = D / 16;       // MFMA k-steps of S^T = K Q^T
+  constexpr int DT = D / 32;       // 32-row tiles of O^T
+  constexpr int KSTR = D + 8;      // bf16 per K row in LDS (+16 B: spreads banks)
+  constexpr int VSTR = AT_KT + 8;  // bf16 per V^T row in LDS
+  constexpr int DSEG = D / 8;      // 16-byte segments per K/V row
+  __shared__ __attribute__((aligned(16))) uint16_t k_s[AT_KT * KSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t vt_s[D * VSTR];
+
+  const int hk = blockIdx.y;
+  const int split = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int r32 = lane & 31;
+  const int hh = lane >> 5;
+  const int per_lane = p.tiles_per_lane * p.g;
+
+  // This wavefront's query tile.
+  const int qt = blockIdx.x * AT_WAVES + w;
+  const bool active = qt < p.q_tiles_kv;
+  int lane_i = 0, c = 0, hg = 0;
+  if (active) {
+    lane_i = qt / per_lane;
+    const int rem = qt - lane_i * per_lane;
+    c = rem / p.g;
+    hg = rem - c * p.g;
+  }
+  const int hq = hk * p.g + hg;
+  const int row0 = lane_i * p.rows_per_lane + c * 32;
+  int nrows = 0;
+  if (active) nrows = min(min(32, p.rows_per_lane - c * 32), p.n_rows - row0);
+  const unsigned long long my_vis = (active && p.n_key_lanes) ? p.vis[lane_i] : 0ull;
+  unsigned long long wg_vis = 0ull;
+  bool wg_active = false;
+  for (int ww = 0; ww < AT_WAVES; ++ww) {
+    const int qt2 = blockIdx.x * AT_WAVES + ww;
+    if (qt2 < p.q_tiles_kv) {
+      wg_active = true;
+      if (p.n_key_lanes) wg_vis |= p.vis[qt2 / per_lane];
+    }
+  }
+  if (!wg_active) return;  // uniform for the workgroup
+
+  // Q fragments (B operand of S^T = K Q^T), kept in registers.
+  bf16x8 qf[KS];
+  {
+    const bool ok = r32 < nrows;
+    const uint16_t* qrow = p.q + ((size_t)(row0 + (ok ? r32 : 0)) * p.Hq + hq) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = ok ? load_bf16x8(qrow + ks * 16 + hh * 8) : zero_bf16x8();
+  }
+
+  f32x16 oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int kt0 = (int)((long long)split * p.total_key_tiles / p.n_split);
+  const int kt1 = (int)((long long)(split + 1) * p.total_key_tiles / p.n_split);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const uint16_t* ksrc;
+    const uint16_t* vsrc;
+    int key_row0, nvalid;
+    bool vis_w;
+    if (kt < p.n_pre_tiles) {
+      key_row0 = kt * AT_KT;
+      nvalid = min(AT_KT, p.P - key_row0);
+      ksrc = p.k_pre;
+      vsrc = p.v_pre;
+      vis_w = active;
+    } else {
+      const int lt = kt - p.n_pre_tiles;
+      const int j = lt / p.lane_key_tiles;
+      const int sub = lt - j * p.lane_key_tiles;
+      if (!((wg_vis >> j) & 1ull)) continue;  // no wavefront here sees block j
+      key_row0 = j * p.B_keys + sub * AT_KT;
+      nvalid = min(AT_KT, p.B_keys - sub * AT_KT);
+      ksrc = p.k_lane;
+      vsrc = p.v_lane;
+      vis_w = active && ((my_vis >> j) & 1ull);
+    }
+
+    __syncthreads();  // the previous tile is no longer read
+    // K tile -> LDS, row-major.
+#pragma unroll
+    for (int i = 0; i < (AT_KT * DSEG) / AT_THREADS; ++i) {
+      const int seg = tid + AT_THREADS * i;
+      const int kr = seg / DSEG;
+      const int ds = seg - kr * DSEG;
+      bf16x8 val = zero_bf16x8();
+      if (kr < nvalid) val = load_bf16x8(ksrc + ((size_t)(key_row0 + kr) * p.Hkv + hk) * D + ds * 8);
+      *reinterpret_cast<bf16x8*>(&k_s[kr * KSTR + ds * 8]) = val;
+    }
+    // V tile -> LDS, transposed ([d][key], permuted key order).
+    for (int pr = tid; pr < (AT_KT / 4) * DSEG; pr += AT_THREADS) {
+      const int k4 = pr / DSEG;
+      const int ds = pr - k4 * DSEG;
+      bf16x8 v4[4];
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) {
+        const int kr = 4 * k4 + c4;
+        v4[c4] = (kr < nvalid)
+                     ? load_bf16x8(vsrc + ((size_t)(key_row0 + kr) * p.Hkv + hk) * D + ds * 8)
+                     : zero_bf16x8();
+      }
+      const int pos = vt_pos4(k4);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        bf16x4 col;
+        col[0] = v4[0][e];
+        col[1] = v4[1][e];
+        col[2] = v4[2][e];
+        col[3] = v4[3][e];
+        *reinterpret_cast<bf16x4*>(&vt_s[(ds * 8 + e) * VSTR + pos]) = col;
+      }
+    }
+    __syncthreads();
+    if (!vis_w) continue;
+
+    const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+      if (kb < nsub) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
+          sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
+        }
+      }
+    }
+    // Scale into log2 units, mask invalid keys, online softmax update.
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        const float x = (key < nvalid) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
+        sacc[kb][r] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, xor32(mx));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2_fast(m_run - m_new);
+    float rs = 0.f;
+    uint16_t pb[2][16];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint16_t b = f32_to_bf16_bits(exp2_fast(sacc[kb][r] - m_new));
+        pb[kb][r] = b;
+        rs += bf16_bits_to_f32(b);
+      }
+    rs += xor32(rs);
+    l_run = l_run * alpha + rs;
+    m_run = m_new;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+
+    // O^T += V^T P^T, one 16-key MFMA step at a time.
+#pragma unroll
+    for (int ks2 = 0; ks2 < 4; ++ks2) {
+      if ((ks2 >> 1) < nsub) {
+        uint16_t bb[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bb[e] = pb[ks2 >> 1][8 * (ks2 & 1) + e];
+        const bf16x8 pbv = __builtin_bit_cast(bf16x8, bb);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&vt_s[(dt * 32 + r32) * VSTR + ks2 * 16 + hh * 8]);
+          oacc[dt] = mfma32x32x16(a, pbv, oacc[dt]);
+        }
+      }
+    }
+  }
+
+  if (!active || r32 >= nrows) return;
+  const size_t orow = (size_t)(row0 + r32) * p.Hq + hq;
+  if (p.n_split == 1) {
+    const float inv_l = 1.0f / l_run;
+    uint16_t* op = p.o + orow * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        uint16_t v4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = f32_to_bf16_bits(oacc[dt][rg * 4 + e] * inv_l);
+        *reinterpret_cast<uint2*>(op + dt * 32 + 8 * rg + 4 * hh) = __builtin_bit_cast(uint2, v4);
+      }
+    if (p.lse && hh == 0) p.lse[orow] = (m_run + log2f(l_run)) * AT_LN2;
+  } else {
+    float* po = p.part_o + ((size_t)split * p.n_rows * p.Hq + orow) * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        float4 v4 = make_float4(oacc[dt][rg * 4 + 0], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2],
+                                oacc[dt][rg * 4 + 3]);
+        *reinterpret_cast<float4*>(po + dt * 32 + 8 * rg + 4 * hh) = v4;
+      }
+    if (hh == 0) {
+      float* pm = p.part_ml + ((size_t)split * p.n_rows * p.Hq + orow) * 2;
+      pm[0] = m_run;
+      pm[1] = l_run;
+    }
+  }
+}
+
+// Combine the key splits of each (row, head): one wavefront per (row, head).
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const float* part_o, const float* part_ml,
+                                                         int n_split, int n_rowheads,
+                                                         uint16_t* o, float* lse) {
+  const int rh = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (rh >= n_rowheads) return;
+  float M = -INFINITY;
+  for (int s = 0; s < n_split; ++s) M = fmaxf(M, part_ml[((size_t)s * n_rowheads + rh) * 2]);
+  float L = 0.f;
+  constexpr int PER = D / 64;
+  float acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  for (int s = 0; s < n_split; ++s) {
+    const float m = part_ml[((size_t)s * n_rowheads + rh) * 2];
+    const float l = part_ml[((size_t)s * n_rowheads + rh) * 2 + 1];
+    const float wgt = (m == -INFINITY) ? 0.f : exp2_fast(m - M);
+    L += l * wgt;
+    const float* po = part_o + ((size_t)s * n_rowheads + rh) * D;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] += po[lane * PER + e] * wgt;
+  }
+  const float inv = 1.0f / L;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) o[(size_t)rh * D + lane * PER + e] = f32_to_bf16_bits(acc[e] * inv);
+  if (lse && lane == 0) lse[rh] = (M + log2f(L)) * AT_LN2;
+}
+
+// Compact-refresh row rewrite: prefix[idx[r]] = ref[r] for K and V.
+__global__ __launch_bounds__(256) void prefix_scatter_kernel(const int32_t* idx, int n_ref,
+                                                             int row_segs, const uint16_t* k_ref,
+                                                             const uint16_t* v_ref, uint16_t* k_pre,
+                                                             uint16_t* v_pre) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long total = (long long)n_ref * row_segs;
+  if (i >= total) return;
+  const int r = (int)(i / row_segs);
+  const int sgi = (int)(i - (long long)r * row_segs);
+  const size_t dst = (size_t)idx[r] * row_segs + sgi;
+  const size_t src = (size_t)r * row_segs + sgi;
+  reinterpret_cast<i32x4*>(k_pre)[dst] = reinterpret_cast<const i32x4*>(k_ref)[src];
+  reinterpret_cast<i32x4*>(v_pre)[dst] = reinterpret_cast<const i32x4*>(v_ref)[src];
+}
+
+// ------------------------------------------------------------------ host
+static int choose_split(int base_wgs, int total_key_tiles) {
+  // Short grids leave most of the 256 CUs idle: split the key tiles (each
+  // split keeps at least two tiles) until about 256 workgroups exist.
+  int s = 1;
+  while (s < 4 && base_wgs * s < 256 && total_key_tiles / (2 * s) >= 2) s *= 2;
+  return s;
+}
+
+struct PassShape {
+  int n_rows, rows_per_lane, tiles_per_lane, q_tiles_kv, base_wgs, n_pre_tiles, total_key_tiles;
+};
+
+static PassShape pass_shape(int n_rows, int rows_per_lane, int n_lanes, int g, int Hkv, int P,
+                            int B_keys, int n_key_lanes) {
+  PassShape s{};
+  s.n_rows = n_rows;
+  s.rows_per_lane = rows_per_lane;
+  s.tiles_per_lane = (rows_per_lane + 31) / 32;
+  s.q_tiles_kv = n_lanes * s.tiles_per_lane * g;
+  s.base_wgs = ((s.q_tiles_kv + AT_WAVES - 1) / AT_WAVES) * Hkv;
+  s.n_pre_tiles = (P + AT_KT - 1) / AT_KT;
+  const int lane_key_tiles = B_keys ? (B_keys + AT_KT - 1) / AT_KT : 0;
+  s.total_key_tiles = s.n_pre_tiles + n_key_lanes * lane_key_tiles;
+  return s;
+}
+
+AttnPlan attn_plan(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
+  AttnPlan pl{};
+  const int g = Hq / Hkv;
+  const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
+  pl.n_split_lane = choose_split(a.base_wgs, a.total_key_tiles);
+  pl.ws_lane = pl.n_split_lane > 1 ? (size_t)pl.n_split_lane * L * B * Hq * (D + 2) * sizeof(float) : 0;
+  pl.n_split_ref = 1;
+  pl.ws_ref = 0;
+  if (n_refresh > 0) {
+    const int nl = (n_refresh + 31) / 32;
+    const PassShape r = pass_shape(n_refresh, 32, nl, g, Hkv, P, 0, 0);
+    pl.n_split_ref = choose_split(r.base_wgs, r.total_key_tiles);
+    pl.ws_ref = pl.n_split_ref > 1 ? (size_t)pl.n_split_ref * n_refresh * Hq * (D + 2) * sizeof(float) : 0;
+  }
+  pl.total = pl.ws_lane > pl.ws_ref ? pl.ws_lane : pl.ws_ref;
+  return pl;
+}
+
+template <int D>
+static hipError_t run_pass(const AttnParams& base, const PassShape& s, int n_split, void* ws,
+                           hipStream_t stream) {
+  AttnParams p = base;
+  p.n_rows = s.n_rows;
+  p.rows_per_lane = s.rows_per_lane;
+  p.tiles_per_lane = s.tiles_per_lane;
+  p.q_tiles_kv = s.q_tiles_kv;
+  p.n_pre_tiles = s.n_pre_tiles;
+  p.total_key_tiles = s.total_key_tiles;
+  p.n_split = n_split;
+  if (n_split > 1) {
+    p.part_o = static_cast<float*>(ws);
+    p.part_ml = p.part_o + (size_t)n_split * s.n_rows * p.Hq * D;
+  }
+  const dim3 grid((s.q_tiles_kv + AT_WAVES - 1) / AT_WAVES, p.Hkv, n_split);
+  hipLaunchKernelGGL(lane_attn_kernel<D>, grid, dim3(AT_THREADS), 0, stream, p);
+  if (n_split > 1) {
+    const int nrh = s.n_rows * p.Hq;
+    hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((nrh + 3) / 4), dim3(256), 0, stream, p.part_o,
+                       p.part_ml, n_split, nrh, p.o, p.lse);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, const uint16_t* v_lane,
+                                 uint16_t* k_pre, uint16_t* v_pre, const unsigned long long* vis,
+                                 int L, int B, int P, int Hq, int Hkv, int D, float scale,
+                                 const int32_t* refresh_idx, int n_refresh, const uint16_t* q_ref,
+                                 const uint16_t* k_ref, const uint16_t* v_ref, uint16_t* o_ref,
+                                 float* lse_ref, uint16_t* o, float* lse, void* ws,
+                                 hipStream_t stream) {
+  const int g = Hq / Hkv;
+  const AttnPlan pl = attn_plan(L, B, P, Hq, Hkv, D, n_refresh);
+  if (n_refresh > 0) {
+    const int row_segs = Hkv * D / 8;
+    const long long total = (long long)n_refresh * row_segs;
+    hipLaunchKernelGGL(prefix_scatter_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                       stream, refresh_idx, n_refresh, row_segs, k_ref, v_ref, k_pre, v_pre);
+  }
+  AttnParams p{};
+  p.Hq = Hq;
+  p.Hkv = Hkv;
+  p.g = g;
+  p.P = P;
+  p.k_pre = k_pre;
+  p.v_pre = v_pre;
+  p.scale_log2 = scale * 1.4426950408889634f;
+
+  // Lane pass.
+  p.q = q;
+  p.k_lane = k_lane;
+  p.v_lane = v_lane;
+  p.o = o;
+  p.lse = lse;
+  p.B_keys = B;
+  p.n_key_lanes = L;
+  p.lane_key_tiles = (B + AT_KT - 1) / AT_KT;
+  for (int i = 0; i < L; ++i) p.vis[i] = vis[i];
+  const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
+  hipError_t e = (D == 64) ? run_pass<64>(p, a, pl.n_split_lane, ws, stream)
+                           : run_pass<128>(p, a, pl.n_split_lane, ws, stream);
+  if (e != hipSuccess || n_refresh <= 0) return e;
+
+  // Refresh pass: refreshed rows over the updated prefix only.
+  AttnParams r = p;
+  r.q = q_ref;
+  r.k_lane = nullptr;
+  r.v_lane = nullptr;
+  r.o = o_ref;
+  r.lse = lse_ref;
+  r.B_keys = 0;
+  r.n_key_lanes = 0;
+  r.lane_key_tiles = 1;
+  for (int i = 0; i < AT_MAX_LANES; ++i) r.vis[i] = 0ull;
+  const int nl = (n_refresh + 31) / 32;
+  const PassShape b = pass_shape(n_refresh, 32, nl, g, Hkv, P, 0, 0);
+  return (D == 64) ? run_pass<64>(r, b, pl.n_split_ref, ws, stream)
+                   : run_pass<128>(r, b, pl.n_split_ref, ws, stream);
+}
+
+}  // namespace al

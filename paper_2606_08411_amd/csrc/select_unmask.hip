@@ -1,0 +1,224 @@
+// Per-lane transfer selection, write-back, ordered compaction and lane
+// boundary statistics for gfx950 -- one workgroup of 16 wavefronts.
+//
+// Paper Section 3.2: each lane applies the block-wise sampler's confidence
+// rule inside its valid update region [0, b_len); transferred positions take
+// their argmax token and are written back; the lane's split point
+// (eq. split_point), fill ratio and step condition (eq. fork_condition) and
+// valid prefix length ("Advancement control") are read on the updated state.
+//
+// The whole step touches a few KB, so it is latency-bound: one workgroup
+// keeps the lane state in LDS, ranks top-k candidates by comparison counting
+// (ties: lower position first), compacts the unmasked / still-masked row
+// lists in order with wavefront ballots, and reduces each lane's statistics
+// with wavefront shuffles.
+#include "common.h"
+#include "launch.h"
+
+namespace al {
+
+constexpr int SEL_THREADS = 1024;
+constexpr int SEL_WAVES = SEL_THREADS / kWave;
+
+struct SelParams {
+  SelHost h;
+  const float* conf;
+  const int32_t* argmax;
+  const int32_t* row_pos;
+  int32_t* tokens;
+  uint8_t* is_masked;
+  uint8_t* unmask_flag;
+  int32_t* unmasked_pos;
+  int32_t* still_pos;
+  int32_t* counts;
+  int32_t* lane_stats;
+  uint8_t* delim_flag;
+};
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p) {
+  __shared__ int s_tok[kSelMaxPositions];
+  __shared__ uint8_t s_msk[kSelMaxPositions];
+  __shared__ uint8_t s_sel[kSelMaxPositions];  // bit0 selected, bit1 candidate
+  __shared__ int s_lo[kSelMaxLanes], s_hi[kSelMaxLanes], s_cnt[kSelMaxLanes], s_nsel[kSelMaxLanes];
+  __shared__ int s_wu[SEL_WAVES], s_ws[SEL_WAVES];
+
+  const SelHost& h = p.h;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int L = h.L, B = h.B, N = h.N, LB = L * B;
+
+  for (int i = tid; i < LB; i += SEL_THREADS) {
+    s_tok[i] = p.tokens[i];
+    s_msk[i] = p.is_masked[i];
+  }
+  if (tid < kSelMaxLanes) {
+    s_lo[tid] = 0;
+    s_hi[tid] = 0;
+    s_cnt[tid] = 0;
+    s_nsel[tid] = 0;
+  }
+  __syncthreads();
+
+  // Candidates, lane row ranges (row_pos is ascending, so each lane's rows
+  // are contiguous) and threshold passes.
+  for (int n = tid; n < N; n += SEL_THREADS) {
+    const int pos = p.row_pos[n];
+    const int ln = pos / B;
+    const int i = pos - ln * B;
+    if (n == 0 || p.row_pos[n - 1] / B != ln) s_lo[ln] = n;
+    if (n == N - 1 || p.row_pos[n + 1] / B != ln) s_hi[ln] = n + 1;
+    const bool cand = i < h.b_len[ln] && s_msk[pos];
+    uint8_t f = cand ? 2 : 0;
+    if (h.mode == 0 && cand && p.conf[n] >= h.tau) {
+      f |= 1;
+      atomicAdd(&s_cnt[ln], 1);
+    }
+    s_sel[n] = f;
+  }
+  __syncthreads();
+
+  // Top-k (TOPK mode) or fallback (THRESHOLD mode, lanes with no pass):
+  // a candidate is chosen when fewer than k candidates of its lane beat it.
+  for (int n = tid; n < N; n += SEL_THREADS) {
+    if (!(s_sel[n] & 2)) continue;
+    const int pos = p.row_pos[n];
+    const int ln = pos / B;
+    const int k = (h.mode == 1) ? h.k_lane[ln] : (s_cnt[ln] == 0 ? h.fallback_k : 0);
+    if (k <= 0) continue;
+    const float c = p.conf[n];
+    int rank = 0;
+    for (int m = s_lo[ln]; m < s_hi[ln]; ++m) {
+      if (!(s_sel[m] & 2)) continue;
+      const float cm = p.conf[m];
+      rank += (cm > c) || (cm == c && p.row_pos[m] < pos);
+    }
+    if (rank < k) s_sel[n] |= 1;
+  }
+  __syncthreads();
+
+  // Write-back.
+  for (int n = tid; n < N; n += SEL_THREADS) {
+    const int sel = s_sel[n] & 1;
+    p.unmask_flag[n] = (uint8_t)sel;
+    if (sel) {
+      const int pos = p.row_pos[n];
+      const int tok = p.argmax[n];
+      p.tokens[pos] = tok;
+      p.is_masked[pos] = 0;
+      s_tok[pos] = tok;
+      s_msk[pos] = 0;
+      atomicAdd(&s_nsel[pos / B], 1);
+    }
+  }
+  __syncthreads();
+
+  // Ordered compaction of transferred / still-masked rows.
+  int base_u = 0, base_s = 0;
+  for (int b0 = 0; b0 < N; b0 += SEL_THREADS) {
+    const int n = b0 + tid;
+    const bool fu = n < N && (s_sel[n] & 1);
+    const bool fs = n < N && !fu && s_msk[p.row_pos[n]];
+    const unsigned long long bu = __ballot(fu);
+    const unsigned long long bs = __ballot(fs);
+    const unsigned long long lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    if (lane == 0) {
+      s_wu[w] = __popcll(bu);
+      s_ws[w] = __popcll(bs);
+    }
+    __syncthreads();
+    int off_u = base_u, off_s = base_s, tot_u = 0, tot_s = 0;
+    for (int ww = 0; ww < SEL_WAVES; ++ww) {
+      if (ww < w) {
+        off_u += s_wu[ww];
+        off_s += s_ws[ww];
+      }
+      tot_u += s_wu[ww];
+      tot_s += s_ws[ww];
+    }
+    if (fu) p.unmasked_pos[off_u + __popcll(bu & lt)] = p.row_pos[n];
+    if (fs) p.still_pos[off_s + __popcll(bs & lt)] = p.row_pos[n];
+    base_u += tot_u;
+    base_s += tot_s;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    p.counts[0] = base_u;
+    p.counts[1] = base_s;
+  }
+
+  // Lane boundary statistics on the updated state: one wavefront per lane.
+  for (int ln = w; ln < L; ln += SEL_WAVES) {
+    const int n = h.b_len[ln];
+    int last = -1, filled = 0, stop = n;
+    for (int i = lane; i < B; i += kWave) {
+      const int pos = ln * B + i;
+      bool isd = false;
+      if (i < n) {
+        const bool m = s_msk[pos] != 0;
+        const int tk = s_tok[pos];
+        if (!m) {
+          ++filled;
+          for (int j = 0; j < h.n_delim; ++j) isd |= (tk == h.delim[j]);
+        }
+        if (isd) last = i;
+        if (m || tk == h.eos_id) stop = min(stop, i);
+      }
+      if (p.delim_flag) p.delim_flag[pos] = (uint8_t)isd;
+    }
+    last = wave_max(last);
+    filled = wave_sum(filled);
+    stop = wave_min(stop);
+    if (lane == 0) {
+      const int split = last + 1;
+      const bool fork = h.role[ln] == 0 && split > 0 &&
+                        (float)filled >= h.rho_min * (float)n && h.t_lane[ln] >= h.t_min;
+      int32_t* st = p.lane_stats + ln * 5;
+      st[0] = split;
+      st[1] = filled;
+      st[2] = stop;
+      st[3] = fork ? 1 : 0;
+      st[4] = s_nsel[ln];
+    }
+  }
+}
+
+hipError_t launch_select(const SelHost& h, const float* conf, const int32_t* argmax,
+                         const int32_t* row_pos, int32_t* tokens, uint8_t* is_masked,
+                         uint8_t* unmask_flag, int32_t* unmasked_pos, int32_t* still_pos,
+                         int32_t* counts, int32_t* lane_stats, uint8_t* delim_flag,
+                         hipStream_t stream) {
+  SelParams p;
+  p.h = h;
+  p.conf = conf;
+  p.argmax = argmax;
+  p.row_pos = row_pos;
+  p.tokens = tokens;
+  p.is_masked = is_masked;
+  p.unmask_flag = unmask_flag;
+  p.unmasked_pos = unmasked_pos;
+  p.still_pos = still_pos;
+  p.counts = counts;
+  p.lane_stats = lane_stats;
+  p.delim_flag = delim_flag;
+  hipLaunchKernelGGL(select_unmask_kernel, dim3(1), dim3(SEL_THREADS), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace al

@@ -11,3 +11,32 @@ if HERE not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+
+
+import pytest  # noqa: E402
+
+
+@pytest.fixture(autouse=True)
+def _announce_gpu_case(request):
+    """Name every GPU test on the real stderr before it touches the device,
+    so a run that ends abruptly still shows which case was running."""
+    if request.node.get_closest_marker("gpu") is not None:
+        sys.__stderr__.write(f"\n[gpu-case] {request.node.nodeid}\n")
+        sys.__stderr__.flush()
+    yield
+
+
+_STEPS = {}
+
+
+@pytest.fixture(scope="session")
+def step_cache():
+    """Synthetic decode steps shared by the tests of one session."""
+    import synth
+
+    def get(name, seed=0, with_weight=True):
+        key = (name, seed, with_weight)
+        if key not in _STEPS:
+            _STEPS[key] = synth.make_step(name, seed, with_weight=with_weight)
+        return _STEPS[key]
+    return get

@@ -254,7 +254,20 @@ def check_refresh(att):
     assert np.abs(out["o"] - o_l).max() < 1e-12
 
 
-ATTENTION_CHECKS = [check_single_lane_is_blockwise, check_chain_is_block_causal,
+def check_rows_agree(att):
+    """The one-row-at-a-time form equals the lane-batched forms."""
+    parent = np.array([-1, 0, 1, 0, 3])
+    L, B, P, Hq, Hkv, D = 5, 4, 6, 4, 2, 8
+    q, kl, vl, kp, vp = _lane_inputs(101, L, B, P, Hq, Hkv, D)
+    ob, lb = att.lane_attention_dense(q, kl, vl, kp, vp, parent, B)
+    rows = [0, 3, 5, 9, 12, 19]
+    heads = [3, 0, 2]
+    o, l = att.lane_attention_rows(q, kl, vl, kp, vp, parent, B, rows, heads)
+    assert np.abs(o - ob[rows][:, heads]).max() < 1e-12
+    assert np.abs(l - lb[rows][:, heads]).max() < 1e-12
+
+
+ATTENTION_CHECKS = [check_single_lane_is_blockwise, check_rows_agree, check_chain_is_block_causal,
                     check_forms_agree, check_v_ones, check_k_zero_mean, check_brute_force,
                     check_prefix_permutation, check_lane_relabel, check_gqa_is_repeated_mha,
                     check_forest_is_independent, check_refresh]

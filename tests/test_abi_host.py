@@ -1,0 +1,106 @@
+"""The C-ABI library on the host: it loads, exports every symbol that
+include/*.h declares, and rejects bad arguments before touching the GPU
+(these calls return from host-side validation; no kernel is launched)."""
+import ctypes
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2606_08411_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2606_08411_amd import build
+        build.build()
+    return _lib.library()
+
+
+def declared_functions():
+    names = []
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        src = open(h).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_][a-z_0-9]*)\s*\(", src, flags=re.M)
+    return sorted(set(names))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"lane_attn_forward", "lmhead_confidence", "select_unmask"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for s in range(-7, 1):
+        assert lib.al_status_string(s)
+    assert lib.al_status_string(-3) == b"lane tree invalid: parent[i] must be in [-1, i)"
+
+
+def test_workspace_sizes(lib):
+    assert lib.lane_attn_workspace_size(4, 32, 512, 32, 32, 128, 0) >= 0
+    assert lib.lane_attn_workspace_size(4, 30, 512, 32, 32, 128, 0) == 0   # B % 16
+    assert lib.lmhead_confidence_workspace_size(77, 4096, 126464) > 0
+    assert lib.lmhead_confidence_workspace_size(0, 4096, 126464) == 0
+    assert lib.lmhead_confidence_workspace_size(5, 12, 100) == 0           # d % 8
+
+
+FAKE = ctypes.c_void_p(1 << 20)      # aligned non-null address, never dereferenced
+
+
+def _attn(lib, parent, L=2, B=32, P=64, Hq=4, Hkv=2, D=64, q=FAKE, o=FAKE, ws=None, wsb=0,
+          ptr=FAKE):
+    par = np.asarray(parent, np.int32)
+    return lib.lane_attn_forward(q, ptr, ptr, ptr, ptr, par.ctypes.data_as(ctypes.c_void_p),
+                                 L, B, P, Hq, Hkv, D, 0.0, None, 0, None, None, None, None, None,
+                                 o, None, ws, wsb, None)
+
+
+def test_attention_validation(lib):
+    assert _attn(lib, [-1, 0], q=None) == -1
+    assert _attn(lib, [-1, 0], B=24) == -2
+    assert _attn(lib, [-1, 0], D=96) == -2
+    assert _attn(lib, [-1, 0], Hq=6, Hkv=4) == -2
+    assert _attn(lib, [-1, 1]) == -3                     # parent[i] must be < i
+    assert _attn(lib, [-2, 0]) == -3
+    assert _attn(lib, [-1, 0], q=ctypes.c_void_p((1 << 20) + 2)) == -5
+    need = lib.lane_attn_workspace_size(2, 32, 4096, 4, 2, 64, 0)
+    if need:
+        assert _attn(lib, [-1, 0], P=4096, ws=FAKE, wsb=need - 1) == -4
+
+
+def test_lmhead_validation(lib):
+    f = lib.lmhead_confidence
+    assert f(FAKE, 10, None, 5, FAKE, 12, 100, None, -1, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
+    assert f(FAKE, 10, None, 11, FAKE, 64, 100, None, -1, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
+    assert f(FAKE, 10, None, 5, FAKE, 64, 100, None, 100, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
+    assert f(None, 10, None, 5, FAKE, 64, 100, None, -1, FAKE, FAKE, None, FAKE, 1 << 30, None) == -1
+    assert f(FAKE, 10, None, 5, FAKE, 64, 100, None, -1, FAKE, FAKE, None, FAKE, 16, None) == -4
+    assert f(FAKE, 10, None, 0, FAKE, 64, 100, None, -1, None, None, None, None, 0, None) == 0
+
+
+def _sel(lib, L=2, B=8, N=4, mode=0, role=(0, 0), b_len=None, k_lane=None, tau=0.9):
+    role = np.asarray(role, np.uint8)
+    bl = None if b_len is None else np.asarray(b_len, np.int32)
+    kl = None if k_lane is None else np.asarray(k_lane, np.int32)
+    delim = np.array([0, 1], np.int32)
+    cp = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+    return lib.select_unmask(FAKE, FAKE, FAKE, N, FAKE, FAKE, L, B, cp(role), cp(bl), None, mode,
+                             tau, 0, cp(kl), cp(delim), 2, 2, 0.5, 2, FAKE, FAKE, FAKE, FAKE,
+                             FAKE, None, None)
+
+
+def test_select_validation(lib):
+    assert _sel(lib, L=0) == -2
+    assert _sel(lib, N=17) == -2
+    assert _sel(lib, L=2, B=8192) == -2
+    assert _sel(lib, mode=1) == -1                        # TOPK needs k_lane
+    assert _sel(lib, role=(0, 3)) == -2
+    assert _sel(lib, b_len=(8, 9)) == -2
+    assert _sel(lib, tau=float("nan")) == -2

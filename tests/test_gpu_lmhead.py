@@ -1,0 +1,113 @@
+"""lmhead_confidence on the GPU against the fp64 oracle.
+
+Rules: argmax must match bit-exactly except on rows whose oracle top-2
+logits differ by less than 1e-3 (several answers are then correct; those
+rows are counted and reported, and must be rare); conf within 2e-2 max abs
+(expected ~1e-5); lse within 2e-3.  Full-size workloads score every masked
+row (LLaDA, Dream) or a seeded sample of rows (Long, Wide).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import dev, dev_bf16, f32
+
+pytestmark = pytest.mark.gpu
+GAP = 1e-3
+TOL_CONF = 2e-2
+TOL_LSE = 2e-3
+
+
+def _run(hidden_bits, W_bits, row_idx, sup, eos_id):
+    import paper_2606_08411_amd as al
+    conf, arg, lse = al.lmhead_confidence(
+        dev_bf16(hidden_bits), dev_bf16(W_bits), row_idx=None if row_idx is None else dev(row_idx),
+        suppress_eos=None if sup is None else dev(sup), eos_id=eos_id)
+    torch.cuda.synchronize()
+    return conf.cpu().numpy(), arg.cpu().numpy(), lse.cpu().numpy()
+
+
+def _compare(gpu, ref, label):
+    conf, arg, lse = gpu
+    ok = ref["gap"] >= GAP
+    excluded = int((~ok).sum())
+    print(f"[{label}] rows={len(arg)} argmax-excluded(gap<{GAP})={excluded} "
+          f"max|dconf|={np.abs(conf - ref['conf']).max():.2e} max|dlse|={np.abs(lse - ref['lse']).max():.2e}")
+    assert np.array_equal(arg[ok], ref["argmax"][ok]), label
+    assert excluded <= max(2, len(arg) // 50)
+    assert np.abs(conf - ref["conf"]).max() < TOL_CONF
+    assert np.abs(lse - ref["lse"]).max() < TOL_LSE
+
+
+@pytest.mark.parametrize("name", ["tiny", "llada", "dream", "long", "wide"])
+def test_lmhead_workloads(name, step_cache):
+    step = step_cache(name, 0)
+    gpu = _run(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
+    sample = np.arange(step.N)
+    if step.N > 128:
+        sample = np.sort(np.random.default_rng([0, 77]).choice(step.N, 48, replace=False))
+    ref = oracle.lmhead.lmhead_confidence_full(
+        f32(step.hidden), step.row_pos[sample], f32(step.W), step.suppress_eos[sample], step.eos_id)
+    _compare(tuple(x[sample] for x in gpu), ref, name)
+
+
+SWEEP = [  # N, n_rows, d, V, eos
+    (1, 1, 8, 1, -1), (1, 3, 8, 2, 1), (5, 9, 64, 7, 3), (33, 40, 264, 1000, 2),
+    (100, 100, 128, 4097, 0), (130, 200, 520, 3000, 17), (300, 310, 64, 513, 2),
+    (64, 64, 1024, 129, -1), (129, 150, 72, 777, 5),
+]
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=[str(c) for c in SWEEP])
+def test_lmhead_sweep(case):
+    N, n_rows, d, V, eos = case
+    g = np.random.default_rng([N, d, V])
+    scale = g.uniform(1, 6, n_rows).astype(np.float32)
+    H = synth.f32_to_bf16_bits(g.standard_normal((n_rows, d), dtype=np.float32) * scale[:, None])
+    W = synth.f32_to_bf16_bits(g.standard_normal((V, d), dtype=np.float32) / np.float32(np.sqrt(d)))
+    row_idx = np.sort(g.choice(n_rows, N, replace=False)).astype(np.int32)[::-1].copy()
+    sup = (g.random(N) < 0.5).astype(np.uint8)
+    gpu = _run(H, W, row_idx, sup, eos)
+    ref = oracle.lmhead.lmhead_confidence_full(f32(H), row_idx, f32(W), sup, eos)
+    _compare(gpu, ref, str(case))
+    if eos >= 0:
+        assert not np.any(gpu[1][sup == 1] == eos)
+
+
+def test_lmhead_zero_weight_and_ties():
+    """W = 0: conf = 1/|C| exactly, argmax = lowest allowed id; duplicated
+    maximal rows: the lower id wins."""
+    N, d, V = 40, 64, 3001
+    g = np.random.default_rng(5)
+    H = synth.f32_to_bf16_bits(g.standard_normal((N, d), dtype=np.float32))
+    W = np.zeros((V, d), np.uint16)
+    sup = np.zeros(N, np.uint8)
+    sup[::2] = 1
+    conf, arg, _ = _run(H, W, None, sup, 0)
+    assert np.array_equal(arg, np.where(sup == 1, 1, 0))
+    assert np.array_equal(conf, np.where(sup == 1, np.float32(1) / np.float32(V - 1),
+                                         np.float32(1) / np.float32(V)).astype(np.float32))
+    # duplicates: rows 100 + 7n and 2000 - 11n both equal 4 * e_(n % d) for row n
+    Hn = np.zeros((N, d), np.float32)
+    Hn[np.arange(N), np.arange(N) % d] = 1.0
+    Wf = g.standard_normal((V, d), dtype=np.float32) * np.float32(0.05)
+    for n in range(N):
+        e = np.zeros(d, np.float32)
+        e[n % d] = 4.0
+        Wf[100 + 7 * n] = e
+        Wf[2000 - 11 * n] = e
+    conf, arg, _ = _run(synth.f32_to_bf16_bits(Hn), synth.f32_to_bf16_bits(Wf), None, None, -1)
+    assert np.array_equal(arg, 100 + 7 * np.arange(N))
+
+
+def test_lmhead_repeatable(step_cache):
+    """Repeated calls (sharing the workspace and its arrival counters) give
+    bitwise-identical results, also after a call with a different shape."""
+    step = step_cache("dream", 0)
+    a = _run(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
+    _run(step.hidden[:40], step.W[:5000], None, None, -1)
+    b = _run(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)

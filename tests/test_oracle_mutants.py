@@ -28,6 +28,9 @@ MUTANTS = {
         ("softmax not normalised", "return p @ v, (m + np.log(l))[:, 0]", "return e @ v, (m + np.log(l))[:, 0]"),
         ("value operand swapped", "return p @ v, (m", "return p @ k, (m"),
         ("lse without max", "return p @ v, (m + np.log(l))[:, 0]", "return p @ v, np.log(l)[:, 0]"),
+        ("row form skips ancestors", "        blocks = anc[i] + [i]\n        for b, h in enumerate(heads):",
+         "        blocks = [i]\n        for b, h in enumerate(heads):"),
+        ("row form modular GQA", "            kv = h // g\n", "            kv = h % Hkv\n"),
         ("refresh writes wrong row", "k2[int(p)] = k_ref[r]", "k2[r] = k_ref[r]"),
         ("refresh rows see their own row only", "o, lse = softmax_attend(q_ref[:, h], k_pre[:, h // g], v_pre[:, h // g], scale)",
          "o, lse = softmax_attend(q_ref[:, h], k_pre[:n, h // g], v_pre[:n, h // g], scale)"),
