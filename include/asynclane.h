@@ -155,18 +155,14 @@ int lane_attn_forward(const al_bf16* q, const al_bf16* k_lane, const al_bf16* v_
  * row_idx  dev [N] int32 or NULL  rows of `hidden` to score (masked positions)
  * N        0..n_rows (N == 0 enqueues nothing)
  * W        dev [V][d]             bf16 LM-head weight (nn.Linear layout)
- * d        multiple of 8, 8..65536;  V: 1..2^30
+ * d        multiple of 8, 8..65536;  n_rows * d < 2^31;  V: 1..2^30
  * suppress_eos dev [N] uint8 or NULL (NULL = no row suppresses EOS)
  * eos_id   in [-1, V); -1 = no EOS id
  * conf, argmax  dev [N] fp32 / int32 out;  lse dev [N] fp32 out or NULL
- * workspace dev, >= lmhead_confidence_workspace_size(N, d, V) bytes.  Its
- *          first 64 KiB hold arrival counters and nothing else, for every
- *          shape: they must be zero before the first call that uses the
- *          workspace (e.g. allocate it zero-filled) and every completed call
- *          leaves them zero again, so one workspace serves calls of any
- *          shape in sequence.  The rest is scratch.  Calls that share a
- *          workspace must not run concurrently.  AL_ERR_UNSUPPORTED when the
- *          counters of a shape would not fit (N beyond ~500k rows).
+ * workspace dev, >= lmhead_confidence_workspace_size(N, d, V) bytes of
+ *          scratch (per-vocab-tile partial maxima, sums and indices);
+ *          contents need not be initialised.  Calls that share a workspace
+ *          must not run concurrently.
  * ------------------------------------------------------------------------ */
 size_t lmhead_confidence_workspace_size(int N, int d, int V);
 

@@ -112,9 +112,7 @@ _ws_cache: dict = {}
 
 
 def _workspace(kind: str, nbytes: int, device, zeroed: bool):
-    """Device workspace cached per (kind, device); grown on demand.  The
-    LM-head workspace is zero-filled once: the library leaves its arrival
-    counters at zero after every call."""
+    """Device workspace cached per (kind, device); grown on demand."""
     if nbytes == 0:
         return None, 0
     key = (kind, str(device))
@@ -199,7 +197,7 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
         return conf, argmax, lse
     need = int(lib.lmhead_confidence_workspace_size(N, d, V))
     if workspace is None:
-        ws, ws_bytes = _workspace("lmhead", need, dev, zeroed=True)
+        ws, ws_bytes = _workspace("lmhead", need, dev, zeroed=False)
     else:
         ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
     st = lib.lmhead_confidence(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,

@@ -104,9 +104,9 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx,
                       float* conf, int32_t* argmax, float* lse, void* workspace,
                       size_t workspace_bytes, void* stream) {
   if (!lm_shape_ok(N, d, V) || n_rows < 0 || N > n_rows) return AL_ERR_SHAPE;
+  if ((long long)n_rows * d >= (1ll << 31)) return AL_ERR_SHAPE;  // 32-bit row offsets
   if (eos_id < -1 || eos_id >= V) return AL_ERR_SHAPE;
   if (N == 0) return AL_OK;
-  if (!al::lmhead_counters_fit(N, V)) return AL_ERR_UNSUPPORTED;
   if (!hidden || !W || !conf || !argmax) return AL_ERR_NULL;
   if (!aligned16(hidden) || !aligned16(W) || !aligned4(conf) || !aligned4(argmax) ||
       (row_idx && !aligned4(row_idx)) || (lse && !aligned4(lse)))

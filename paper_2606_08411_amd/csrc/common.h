@@ -21,6 +21,13 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// D[16x16] += A[16x32] * B[32x16] in bf16 with fp32 accumulation.
+// Lane l holds A[l%16][8*(l/16) + e], B[8*(l/16) + e][l%16] (e = 0..7) and
+// D[4*(l/16) + r][l%16] in register r = 0..3.
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // fp32 -> bf16 round-to-nearest-even (finite inputs).

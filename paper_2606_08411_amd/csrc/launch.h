@@ -23,7 +23,6 @@ hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, cons
 
 // ---- LM head
 size_t lmhead_workspace_bytes(int N, int d, int V);
-bool lmhead_counters_fit(int N, int V);
 hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N, const uint16_t* W,
                          int d, int V, const uint8_t* sup, int eos_id, float* conf,
                          int32_t* argmax, float* lse, void* ws, hipStream_t stream);

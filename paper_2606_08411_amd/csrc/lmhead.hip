@@ -1,20 +1,31 @@
 // Fused LM head + confidence for gfx950.
 //
-// For each scored hidden row n the kernel forms z[v] = <H[row_idx[n]], W[v]>
-// on bf16 MFMA with fp32 accumulation and reduces every vocabulary tile to a
-// running (max m, sum s = sum exp(z - m), first argmax) triple in registers,
-// so the logits never reach memory (paper Section 3.2: confidence-based
-// transfer uses the max-probability token of each masked position; refine
-// lanes suppress EOS).
+// For each scored hidden row n the kernels form z[v] = <H[row_idx[n]], W[v]>
+// on bf16 MFMA with fp32 accumulation and reduce every vocabulary tile to a
+// (max m, sum s = sum exp(z - m), first argmax) triple in registers, so the
+// logits never reach memory (paper Section 3.2: confidence-based transfer
+// uses the max-probability token of each masked position; refine lanes
+// suppress EOS).
 //
-// Work split.  A workgroup (4 wavefronts) owns 128 vocabulary rows (32 per
-// wavefront) and one tile of up to 128 hidden rows ("columns").  W is
-// streamed from HBM exactly once, straight into registers (each W element is
-// used by one wavefront only); the hidden-row chunk is staged once per
-// workgroup in LDS and shared by the four wavefronts.  The vocabulary tiles
-// of one column tile are merged in a fixed order by the last workgroup to
-// arrive (two levels of arrival counters), so one launch produces the final
-// conf / argmax / lse and the result is bitwise reproducible.
+// The step streams the whole weight W ([V][d] bf16, ~1 GB at V=126464,
+// d=4096) once for a few hundred hidden rows, so lmhead_partial_kernel is
+// shaped for HBM streaming rather than for MFMA reuse (measured on MI355X):
+// * each wavefront owns 16 vocabulary rows (the A operand of the 16x16x32
+//   bf16 MFMA); per chunk it loads 256 contiguous bytes of each row
+//   (4 lanes x 64 B, issued back to back) straight into registers, one
+//   chunk ahead of the MFMAs -- each W element is used by one wavefront;
+// * the K index inside a chunk is permuted identically on W and H so each
+//   lane's 128 B run maps onto consecutive MFMA k-steps;
+// * the chunk of the scored hidden rows (B operand, <= 128 rows) is staged
+//   once per workgroup in LDS and shared by its wavefronts; the LDS buffer
+//   is small enough for several workgroups per CU, which keeps enough W
+//   loads in flight;
+// * workgroups are dealt to the 8 XCDs in contiguous runs of vocab tiles;
+// * the epilogue writes one partial (m, s, argmax) per column and vocab
+//   tile; lmhead_merge_kernel combines them in a fixed order, so results
+//   are bitwise reproducible.  (A single-kernel merge by the last workgroup
+//   to arrive needs agent-scope fences, which on gfx950 write back and
+//   invalidate the L2 in every workgroup; the separate launch is cheaper.)
 #include <math.h>
 
 #include "common.h"
@@ -22,13 +33,7 @@
 
 namespace al {
 
-constexpr int LM_WAVES = 4;
-constexpr int LM_THREADS = LM_WAVES * kWave;
-constexpr int LM_VT = 32 * LM_WAVES;        // vocabulary rows per workgroup
-constexpr int LM_KC = 64;                   // K (hidden) elements per chunk
-constexpr int LM_LDS_STRIDE = LM_KC + 8;    // bf16 per staged hidden row (+16 B pad)
-constexpr int LM_MIN_GROUP = 16;            // vocab tiles merged by one level-1 merger
-constexpr size_t LM_CNT_BYTES = 65536;      // arrival-counter area at the workspace start
+constexpr int LM_MAX_FRAG = 8;   // <= 128 scored rows per column tile
 constexpr float LM_LOG2E = 1.4426950408889634f;
 
 struct LmPartial {
@@ -43,19 +48,13 @@ struct LmParams {
   const int32_t* row_idx;
   const uint16_t* W;
   const uint8_t* sup;
-  float* conf;
-  int32_t* argmax;
-  float* lse;
-  LmPartial* part;    // [n_nt][n_vt][NT]
-  LmPartial* gpart;   // [n_nt][n_groups][NT]
-  unsigned* cnt1;     // [n_nt][n_groups]
-  unsigned* cnt2;     // [n_nt]
+  LmPartial* part;  // [n_nt][n_vt][nt_cols]
   int N, d, V, eos_id;
-  int n_vt, n_nt, n_groups, group, tiles_total, tiles_per_xcd;
+  int n_vt, n_nt, nt_cols, tiles_total, tiles_per_xcd;
 };
 
 // Merge (m2, s2, i2) into (m, s, i): max, rescaled sum, lowest index on ties.
-// Commutative, so both halves of a lane pair obtain identical bits.
+// Commutative, so lanes that exchange states obtain identical bits.
 __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float m2, float s2,
                                             int idx2) {
   if (m2 == -INFINITY) return;
@@ -71,19 +70,29 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
   m = M;
 }
 
-template <int NB>
-__global__ __launch_bounds__(LM_THREADS) __attribute__((amdgpu_waves_per_eu(3, 4)))
-void lmhead_conf_kernel(LmParams p) {
-  constexpr int NT = 32 * NB;
-  __shared__ __attribute__((aligned(16))) uint16_t hs[2][NT * LM_LDS_STRIDE];
-  __shared__ float red_m[LM_WAVES][NT];
-  __shared__ float red_s[LM_WAVES][NT];
-  __shared__ int red_i[LM_WAVES][NT];
-  __shared__ unsigned s_ticket;
+// WAVES wavefronts x 16 vocab rows per workgroup; KC hidden elements per
+// chunk (each lane streams KC/4 contiguous elements of its row per chunk).
+// OCC: wavefronts per SIMD the register allocation must allow.
+template <int NFRAG, bool RAGGED, int WAVES, int KC, int OCC>
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+void lmhead_partial_kernel(LmParams p) {
+  constexpr int THREADS = WAVES * 64;
+  constexpr int VT = 16 * WAVES;                 // vocab rows per workgroup
+  constexpr int LANE_K = KC / 4;                 // contiguous K per lane per chunk
+  constexpr int STEPS = LANE_K / 8;              // MFMA k-steps per chunk
+  constexpr int NT = 16 * NFRAG;                 // scored rows (columns) per tile
+  constexpr int KSEG = KC / 8;                   // 16-byte segments per staged row
+  constexpr int STRIDE = KC + 8;                 // bf16 per staged row (+16 B pad)
+  constexpr int RPP = THREADS / KSEG;            // staged rows per pass
+  constexpr int HREG = (NT + RPP - 1) / RPP;
+  constexpr int ROWS_STAGED = HREG * RPP;        // >= NT; extra rows unused
+  __shared__ __attribute__((aligned(16))) uint16_t hs[ROWS_STAGED * STRIDE];
+  // After the K loop the staging buffer holds the per-wavefront (m, s, idx).
+  static_assert(sizeof(hs) >= 3 * sizeof(float) * WAVES * NT, "reduction scratch");
+  float (*red_m)[NT] = reinterpret_cast<float (*)[NT]>(&hs[0]);
+  float (*red_s)[NT] = red_m + WAVES;
+  int (*red_i)[NT] = reinterpret_cast<int (*)[NT]>(red_s + WAVES);
 
-  // XCD-aware tile order: blocks are dealt round-robin to the 8 XCDs, so
-  // give each XCD a contiguous run of tiles (the column tiles of one vocab
-  // tile then share that XCD's L2 while their W rows are hot).
   const int b = blockIdx.x;
   const int t = (b & 7) * p.tiles_per_xcd + (b >> 3);
   if (t >= p.tiles_total) return;
@@ -93,210 +102,210 @@ void lmhead_conf_kernel(LmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
-  const int r32 = lane & 31;
-  const int hh = lane >> 5;
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
   const int d = p.d;
-  const int v0 = vt * LM_VT + w * 32;
-  const int n0 = nt * NT;
+  const int v0 = vt * VT + w * 16;
+  const int n0 = nt * p.nt_cols;
+  const int ncols = min(NT, p.N - n0);
 
-  const uint16_t* wrow = p.W + (size_t)min(v0 + r32, p.V - 1) * d;
-
-  // Hidden-row staging: NT rows x 8 segments of 8 bf16 per chunk; thread
-  // tid moves segments tid + 256*i.
-  const uint16_t* hsrc[NB];
-  int hdst[NB];
-  int hk[NB];
-  bool hok[NB];
+  // Loads are unconditional and in bounds (clamped addresses); values are
+  // not post-processed after loading.  A W segment past d meets hidden
+  // values zeroed at the LDS store; rows past V are dropped in the epilogue.
+  const uint16_t* wrow = p.W + (size_t)min(v0 + r16, p.V - 1) * d;
+  const uint16_t* wlane = wrow + g4 * LANE_K;
+  const int hk = (tid % KSEG) * 8;
+  // Row offsets into `hidden` (32-bit: n_rows * d < 2^31 is checked).
+  unsigned hrow[HREG];
+  unsigned hvalid = 0;
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int seg = tid + LM_THREADS * i;
-    const int row = seg >> 3;
-    const int kseg = seg & 7;
-    const int n = n0 + row;
-    hok[i] = n < p.N;
-    const int r = hok[i] ? (p.row_idx ? p.row_idx[n] : n) : 0;
-    hsrc[i] = p.hidden + (size_t)r * d + kseg * 8;
-    hk[i] = kseg * 8;
-    hdst[i] = row * LM_LDS_STRIDE + kseg * 8;
+  for (int i = 0; i < HREG; ++i) {
+    const int row = tid / KSEG + RPP * i;
+    const bool ok = row < ncols;
+    const int n = n0 + (ok ? row : 0);
+    hrow[i] = (unsigned)(p.row_idx ? p.row_idx[n] : n) * (unsigned)d + (unsigned)hk;
+    hvalid |= (ok ? 1u : 0u) << i;
   }
+  const int hdst0 = (tid / KSEG) * STRIDE + hk;
 
-  bf16x8 wc[4], wn[4], hr[NB];
-  auto load_w = [&](bf16x8* dst, int kc) {
+  f32x4 acc[NFRAG];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int k = kc + s * 16 + hh * 8;
-      dst[s] = (k < d) ? load_bf16x8(wrow + k) : zero_bf16x8();
+  for (int f = 0; f < NFRAG; ++f)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[f][r] = 0.f;
+
+  bf16x8 wa[STEPS], wb[STEPS], hr[HREG];
+  auto load_w = [&](bf16x8* wv, int kc) {
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      if (RAGGED) {
+        const int k = kc + g4 * LANE_K + s * 8;
+        wv[s] = load_bf16x8(wrow + (k < d ? k : 0));
+      } else {
+        wv[s] = load_bf16x8(wlane + kc + s * 8);
+      }
     }
   };
   auto load_h = [&](int kc) {
+    const bool kin = !RAGGED || kc + hk < d;
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-      hr[i] = (hok[i] && kc + hk[i] < d) ? load_bf16x8(hsrc[i] + kc) : zero_bf16x8();
+    for (int i = 0; i < HREG; ++i) hr[i] = load_bf16x8(p.hidden + (hrow[i] + (kin ? kc : -hk)));
   };
-  auto store_h = [&](int buf) {
+  // Zeroing past d and for unused columns happens at the LDS store, where
+  // the data is awaited anyway (a select right after a load would stall).
+  auto store_h = [&](int kc) {
+    const bool kin = !RAGGED || kc + hk < d;
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-      *reinterpret_cast<bf16x8*>(&hs[buf][hdst[i]]) = hr[i];
+    for (int i = 0; i < HREG; ++i)
+      *reinterpret_cast<bf16x8*>(&hs[hdst0 + RPP * i * STRIDE]) =
+          (kin && ((hvalid >> i) & 1u)) ? hr[i] : zero_bf16x8();
   };
-
-  f32x16 acc[NB];
+  // MFMA step s covers, for lane group g4, the K elements
+  // kc + g4*LANE_K + s*8 + e (e = 0..7) on both operands.
+  auto mma = [&](const bf16x8* wv) {
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+    for (int s = 0; s < STEPS; ++s) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
-
-  const int nch = (d + LM_KC - 1) / LM_KC;
-  load_h(0);
-  load_w(wc, 0);
-  store_h(0);
-  __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    const int buf = c & 1;
-    const bool more = c + 1 < nch;
-    if (more) {
-      load_h((c + 1) * LM_KC);
-      load_w(wn, (c + 1) * LM_KC);
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(
-            &hs[buf][(nb * 32 + r32) * LM_LDS_STRIDE + s * 16 + hh * 8]);
-        acc[nb] = mfma32x32x16(wc[s], bv, acc[nb]);
+      for (int f = 0; f < NFRAG; ++f) {
+        const bf16x8 bv =
+            *reinterpret_cast<const bf16x8*>(&hs[(f * 16 + r16) * STRIDE + g4 * LANE_K + s * 8]);
+        acc[f] = mfma16x16x32(wv[s], bv, acc[f]);
       }
     }
-    if (more) store_h(buf ^ 1);
+  };
+  // One chunk whose successor exists: load the next hidden chunk, then
+  // prefetch W(next) -- in that order, because the LDS store waits for the
+  // hidden loads and the load counter is in-order -- multiply, restage LDS.
+  auto step = [&](const bf16x8* cur, bf16x8* nxt, int kc_next) {
+    load_h(kc_next);
+    load_w(nxt, kc_next);
+    // Keep the prefetch loads ahead of the MFMAs (the scheduler would
+    // otherwise sink them and shorten the prefetch distance).
+    __builtin_amdgcn_sched_barrier(0);
+    mma(cur);
+    __syncthreads();  // every wavefront is done with this hidden chunk
+    store_h(kc_next);
     __syncthreads();
-#pragma unroll
-    for (int s = 0; s < 4; ++s) wc[s] = wn[s];
-  }
+  };
 
-  // Epilogue: each lane holds 16 vocab rows of column n0 + nb*32 + r32.
+  // W chunk c+1 is in flight while chunk c is multiplied; registers
+  // ping-pong between wa (even chunks) and wb (odd chunks) without copies.
+  // The steady-state loop has no tail conditions; the last chunk is peeled.
+  const int nch = (d + KC - 1) / KC;
+  load_h(0);
+  load_w(wa, 0);
+  store_h(0);
+  __syncthreads();
+  int c = 0;
+  for (; c + 2 < nch; c += 2) {
+    step(wa, wb, (c + 1) * KC);
+    step(wb, wa, (c + 2) * KC);
+  }
+  if (c + 1 < nch) {
+    step(wa, wb, (c + 1) * KC);
+    mma(wb);
+  } else {
+    mma(wa);
+  }
+  __syncthreads();
+
+  // Epilogue: lane (r16, g4) holds vocab rows v0 + 4*g4 + r (r = 0..3) of
+  // column n0 + f*16 + r16.
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int n = n0 + nb * 32 + r32;
+  for (int f = 0; f < NFRAG; ++f) {
+    const int n = n0 + f * 16 + r16;
     const bool sup_row = (n < p.N) && p.sup && p.sup[n];
     float m = -INFINITY;
     int idx = 0x7fffffff;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int v = v0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+    for (int r = 0; r < 4; ++r) {
+      const int v = v0 + 4 * g4 + r;
       const bool ok = v < p.V && !(sup_row && v == p.eos_id);
-      if (ok && acc[nb][r] > m) {
-        m = acc[nb][r];
+      if (ok && acc[f][r] > m) {
+        m = acc[f][r];
         idx = v;
       }
     }
     float s = 0.f;
     if (m != -INFINITY) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = v0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      for (int r = 0; r < 4; ++r) {
+        const int v = v0 + 4 * g4 + r;
         const bool ok = v < p.V && !(sup_row && v == p.eos_id);
-        if (ok) s += exp2_fast((acc[nb][r] - m) * LM_LOG2E);
+        if (ok) s += exp2_fast((acc[f][r] - m) * LM_LOG2E);
       }
     }
-    merge_state(m, s, idx, xor32(m), xor32(s), xor32(idx));
-    if (hh == 0) {
-      red_m[w][nb * 32 + r32] = m;
-      red_s[w][nb * 32 + r32] = s;
-      red_i[w][nb * 32 + r32] = idx;
+    merge_state(m, s, idx, __shfl_xor(m, 16, kWave), __shfl_xor(s, 16, kWave),
+                __shfl_xor(idx, 16, kWave));
+    merge_state(m, s, idx, __shfl_xor(m, 32, kWave), __shfl_xor(s, 32, kWave),
+                __shfl_xor(idx, 32, kWave));
+    if (g4 == 0) {
+      red_m[w][f * 16 + r16] = m;
+      red_s[w][f * 16 + r16] = s;
+      red_i[w][f * 16 + r16] = idx;
     }
   }
   __syncthreads();
-  if (tid < NT) {
-    float m = red_m[0][tid], s = red_s[0][tid];
-    int idx = red_i[0][tid];
+  for (int col = tid; col < NT; col += THREADS) {
+    float m = red_m[0][col], s = red_s[0][col];
+    int idx = red_i[0][col];
+    for (int ww = 1; ww < WAVES; ++ww) merge_state(m, s, idx, red_m[ww][col], red_s[ww][col], red_i[ww][col]);
+    LmPartial q;
+    q.m = m;
+    q.s = s;
+    q.idx = idx;
+    q.pad = 0;
+    p.part[((size_t)nt * p.n_vt + vt) * p.nt_cols + col] = q;
+  }
+}
+
+// One wavefront per scored row: lanes merge strided runs of vocab-tile
+// partials in ascending order, then a fixed xor-butterfly combines lanes.
+__global__ __launch_bounds__(256) void lmhead_merge_kernel(const LmPartial* part, int N, int n_vt,
+                                                           int nt_cols, float* conf, int32_t* argmax,
+                                                           float* lse) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const int nt = n / nt_cols;
+  const int col = n - nt * nt_cols;
+  const LmPartial* base = part + (size_t)nt * n_vt * nt_cols + col;
+  float m = -INFINITY, s = 0.f;
+  int idx = 0x7fffffff;
+  for (int v = lane; v < n_vt; v += kWave) {
+    const LmPartial q = base[(size_t)v * nt_cols];
+    merge_state(m, s, idx, q.m, q.s, q.idx);
+  }
 #pragma unroll
-    for (int ww = 1; ww < LM_WAVES; ++ww) merge_state(m, s, idx, red_m[ww][tid], red_s[ww][tid], red_i[ww][tid]);
-    LmPartial q;
-    q.m = m;
-    q.s = s;
-    q.idx = idx;
-    q.pad = 0;
-    p.part[((size_t)nt * p.n_vt + vt) * NT + tid] = q;
+  for (int o = 1; o < kWave; o <<= 1)
+    merge_state(m, s, idx, __shfl_xor(m, o, kWave), __shfl_xor(s, o, kWave), __shfl_xor(idx, o, kWave));
+  if (lane == 0) {
+    conf[n] = 1.0f / s;
+    argmax[n] = idx;
+    if (lse) lse[n] = m + logf(s);
   }
-
-  // ---- level 1: the last vocab tile of a group to arrive merges the group.
-  const int g = vt / p.group;
-  const int g_lo = g * p.group;
-  const int g_hi = min(g_lo + p.group, p.n_vt);
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_ticket = atomicAdd(&p.cnt1[nt * p.n_groups + g], 1u);
-  __syncthreads();
-  if (s_ticket != (unsigned)(g_hi - g_lo - 1)) return;
-  __threadfence();
-  if (tid < NT) {
-    float m = -INFINITY, s = 0.f;
-    int idx = 0x7fffffff;
-    for (int v = g_lo; v < g_hi; ++v) {
-      const LmPartial q = p.part[((size_t)nt * p.n_vt + v) * NT + tid];
-      merge_state(m, s, idx, q.m, q.s, q.idx);
-    }
-    LmPartial q;
-    q.m = m;
-    q.s = s;
-    q.idx = idx;
-    q.pad = 0;
-    p.gpart[((size_t)nt * p.n_groups + g) * NT + tid] = q;
-  }
-  if (tid == 0) atomicExch(&p.cnt1[nt * p.n_groups + g], 0u);
-
-  // ---- level 2: the last group merger of this column tile finishes it.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_ticket = atomicAdd(&p.cnt2[nt], 1u);
-  __syncthreads();
-  if (s_ticket != (unsigned)(p.n_groups - 1)) return;
-  __threadfence();
-  if (tid < NT) {
-    const int n = n0 + tid;
-    if (n < p.N) {
-      float m = -INFINITY, s = 0.f;
-      int idx = 0x7fffffff;
-      for (int gg = 0; gg < p.n_groups; ++gg) {
-        const LmPartial q = p.gpart[((size_t)nt * p.n_groups + gg) * NT + tid];
-        merge_state(m, s, idx, q.m, q.s, q.idx);
-      }
-      p.conf[n] = 1.0f / s;
-      p.argmax[n] = idx;
-      if (p.lse) p.lse[n] = m + logf(s);
-    }
-  }
-  if (tid == 0) atomicExch(&p.cnt2[nt], 0u);
 }
 
 // ------------------------------------------------------------------ host
-static int lm_nb(int N) { return N >= 128 ? 4 : (N + 31) / 32; }
+constexpr int LM_WAVES = 8;
+constexpr int LM_KC = 128;
+constexpr int LM_OCC = 4;
+constexpr int LM_VT = 16 * LM_WAVES;
 
-// Workspace: [0, 64 KiB) holds only the arrival counters (cnt1 then cnt2),
-// whatever the shape, so counters left at zero by any completed call are
-// still zero for the next call even when the shape changes.  Partials
-// follow.  The level-1 group grows when the counters would not fit.
+// Column tiling: n_nt tiles of nfrag 16-column fragments (<= 128 columns).
 struct LmLayout {
-  int nb, nt_cols, n_nt, n_vt, n_groups, group;
-  size_t off_cnt2, off_part, off_gpart, total;
+  int nfrag, nt_cols, n_nt, n_vt;
+  size_t total;
 };
 
 static LmLayout lm_layout(int N, int V) {
   LmLayout L{};
-  L.nb = N > 0 ? lm_nb(N) : 1;
-  L.nt_cols = 32 * L.nb;
-  L.n_nt = N > 0 ? (N + L.nt_cols - 1) / L.nt_cols : 0;
+  const int frags = N > 0 ? (N + 15) / 16 : 1;
+  L.n_nt = N > 0 ? (frags + LM_MAX_FRAG - 1) / LM_MAX_FRAG : 0;
+  L.nfrag = N > 0 ? (frags + L.n_nt - 1) / L.n_nt : 1;
+  L.nt_cols = 16 * L.nfrag;
   L.n_vt = (V + LM_VT - 1) / LM_VT;
-  const size_t max_cnt = LM_CNT_BYTES / sizeof(unsigned);
-  L.group = LM_MIN_GROUP;
-  for (;;) {
-    L.n_groups = (L.n_vt + L.group - 1) / L.group;
-    if ((size_t)L.n_nt * (L.n_groups + 1) <= max_cnt || L.group >= L.n_vt) break;
-    L.group *= 2;
-  }
-  L.off_cnt2 = sizeof(unsigned) * (size_t)L.n_nt * L.n_groups;
-  L.off_part = LM_CNT_BYTES;
-  L.off_gpart = L.off_part + sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
-  L.total = L.off_gpart + sizeof(LmPartial) * (size_t)L.n_nt * L.n_groups * L.nt_cols;
+  L.total = sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
   return L;
 }
 
@@ -304,11 +313,6 @@ size_t lmhead_workspace_bytes(int N, int d, int V) {
   (void)d;
   if (N <= 0 || V <= 0) return 0;
   return lm_layout(N, V).total;
-}
-
-bool lmhead_counters_fit(int N, int V) {
-  const LmLayout L = lm_layout(N, V);
-  return (size_t)L.n_nt * (L.n_groups + 1) * sizeof(unsigned) <= LM_CNT_BYTES;
 }
 
 hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
@@ -322,31 +326,41 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.row_idx = row_idx;
   p.W = W;
   p.sup = sup;
-  p.conf = conf;
-  p.argmax = argmax;
-  p.lse = lse;
-  char* base = static_cast<char*>(ws);
-  p.cnt1 = reinterpret_cast<unsigned*>(base);
-  p.cnt2 = reinterpret_cast<unsigned*>(base + L.off_cnt2);
-  p.part = reinterpret_cast<LmPartial*>(base + L.off_part);
-  p.gpart = reinterpret_cast<LmPartial*>(base + L.off_gpart);
+  p.part = static_cast<LmPartial*>(ws);
   p.N = N;
   p.d = d;
   p.V = V;
   p.eos_id = eos_id;
   p.n_vt = L.n_vt;
   p.n_nt = L.n_nt;
-  p.n_groups = L.n_groups;
-  p.group = L.group;
+  p.nt_cols = L.nt_cols;
   p.tiles_total = L.n_vt * L.n_nt;
   p.tiles_per_xcd = (p.tiles_total + 7) / 8;
-  const dim3 grid(8 * p.tiles_per_xcd), block(LM_THREADS);
-  switch (L.nb) {
-    case 1: hipLaunchKernelGGL(lmhead_conf_kernel<1>, grid, block, 0, stream, p); break;
-    case 2: hipLaunchKernelGGL(lmhead_conf_kernel<2>, grid, block, 0, stream, p); break;
-    case 3: hipLaunchKernelGGL(lmhead_conf_kernel<3>, grid, block, 0, stream, p); break;
-    default: hipLaunchKernelGGL(lmhead_conf_kernel<4>, grid, block, 0, stream, p); break;
+  const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
+  const bool ragged = d % LM_KC != 0;
+#define AL_LM_CASE(F)                                                                         \
+  case F:                                                                                     \
+    if (ragged)                                                                               \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, LM_OCC>), grid, block, 0,  \
+                         stream, p);                                                          \
+    else                                                                                      \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, LM_OCC>), grid, block, 0, \
+                         stream, p);                                                          \
+    break;
+  switch (L.nfrag) {
+    AL_LM_CASE(1)
+    AL_LM_CASE(2)
+    AL_LM_CASE(3)
+    AL_LM_CASE(4)
+    AL_LM_CASE(5)
+    AL_LM_CASE(6)
+    AL_LM_CASE(7)
+    default:
+      AL_LM_CASE(8)
   }
+#undef AL_LM_CASE
+  hipLaunchKernelGGL(lmhead_merge_kernel, dim3((N + 3) / 4), dim3(256), 0, stream, p.part, N,
+                     L.n_vt, L.nt_cols, conf, argmax, lse);
   return hipGetLastError();
 }
 
