@@ -5,8 +5,9 @@ them) + lmhead_confidence over the masked positions + select_unmask, on
 seeded synthetic inputs already resident in HBM.  Prints ONE JSON line.
 
 value       (attention FLOPs + LM-head FLOPs) / step time, in TFLOP/s
-roofline    the LM-head kernel (the step's dominant kernel) against HBM:
-            algorithmic bytes per launch / its measured average duration
+roofline    the LM-head call (the step's dominant op: a streaming GEMM
+            kernel + a small merge kernel) against HBM: algorithmic bytes
+            per call / its measured average duration
 cpu_baseline the fp64 oracle on a bounded sample of the same workload,
             timed on this host's cores
 """
@@ -82,10 +83,10 @@ def kernel_source_hash():
 
 
 def measured_traffic(config):
-    """HBM bytes per launch of the LM-head kernel from the committed
+    """HBM bytes per LM-head call (both kernels) from the committed
     rocprofv3 counter summary, or None when it is missing or was taken on
     another version of the kernel source."""
-    path = os.path.join(ROOT, "profiles", f"lmhead_conf_kernel_{config}_pmc.json")
+    path = os.path.join(ROOT, "profiles", f"lmhead_confidence_{config}_pmc.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -257,7 +258,7 @@ def main():
         "attention_tflops": round(f_attn / (t_attn * 1e-3) / 1e12, 2),
         "lmhead_tflops": round(f_lm / (t_lm * 1e-3) / 1e12, 2),
         "roofline": {
-            "kernel": "lmhead_conf_kernel",
+            "kernel": "lmhead_confidence (lmhead_partial_kernel + lmhead_merge_kernel)",
             "bound": "hbm",
             "achieved": round(lm_gbs, 1),
             "peak": PEAK_HBM_GBS,

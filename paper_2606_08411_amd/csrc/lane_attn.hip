@@ -123,55 +123,93 @@ __global__ __launch_bounds__(AT_THREADS) void lane_attn_kernel(AttnParams p) {
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
+  // Key tiles of this split: prefix tiles, then lane-block tiles.  Tiles no
+  // wavefront of the workgroup sees are skipped (uniformly).
   const int kt0 = (int)((long long)split * p.total_key_tiles / p.n_split);
   const int kt1 = (int)((long long)(split + 1) * p.total_key_tiles / p.n_split);
-  for (int kt = kt0; kt < kt1; ++kt) {
-    const uint16_t* ksrc;
-    const uint16_t* vsrc;
-    int key_row0, nvalid;
-    bool vis_w;
-    if (kt < p.n_pre_tiles) {
-      key_row0 = kt * AT_KT;
-      nvalid = min(AT_KT, p.P - key_row0);
-      ksrc = p.k_pre;
-      vsrc = p.v_pre;
-      vis_w = active;
-    } else {
+  struct Tile {
+    const uint16_t* k;  // first key row of the tile, K/V head hk applied
+    const uint16_t* v;
+    int nvalid;         // valid keys (1..64); 0 = no tile
+    bool vis;           // this wavefront attends to it
+  };
+  auto tile_at = [&](int kt) -> Tile {
+    Tile tl{nullptr, nullptr, 0, false};
+    for (; kt < kt1; ++kt) {
+      if (kt < p.n_pre_tiles) {
+        const int r0 = kt * AT_KT;
+        tl.k = p.k_pre + ((size_t)r0 * p.Hkv + hk) * D;
+        tl.v = p.v_pre + ((size_t)r0 * p.Hkv + hk) * D;
+        tl.nvalid = min(AT_KT, p.P - r0);
+        tl.vis = active;
+        return tl;
+      }
       const int lt = kt - p.n_pre_tiles;
       const int j = lt / p.lane_key_tiles;
       const int sub = lt - j * p.lane_key_tiles;
-      if (!((wg_vis >> j) & 1ull)) continue;  // no wavefront here sees block j
-      key_row0 = j * p.B_keys + sub * AT_KT;
-      nvalid = min(AT_KT, p.B_keys - sub * AT_KT);
-      ksrc = p.k_lane;
-      vsrc = p.v_lane;
-      vis_w = active && ((my_vis >> j) & 1ull);
+      if (!((wg_vis >> j) & 1ull)) continue;
+      const int r0 = j * p.B_keys + sub * AT_KT;
+      tl.k = p.k_lane + ((size_t)r0 * p.Hkv + hk) * D;
+      tl.v = p.v_lane + ((size_t)r0 * p.Hkv + hk) * D;
+      tl.nvalid = min(AT_KT, p.B_keys - sub * AT_KT);
+      tl.vis = active && ((my_vis >> j) & 1ull);
+      return tl;
     }
+    return tl;
+  };
+  auto next_kt = [&](int kt) {  // index after the tile found from kt
+    for (; kt < kt1; ++kt) {
+      if (kt < p.n_pre_tiles) return kt + 1;
+      const int j = (kt - p.n_pre_tiles) / p.lane_key_tiles;
+      if ((wg_vis >> j) & 1ull) return kt + 1;
+    }
+    return kt1;
+  };
 
-    __syncthreads();  // the previous tile is no longer read
-    // K tile -> LDS, row-major.
+  // Register staging of one tile: K as KREG 16-byte row segments, V as
+  // 4 keys x 8 d blocks (for the transposed LDS copy).
+  constexpr int KREG = (AT_KT * DSEG) / AT_THREADS;
+  constexpr int VPAIRS = (AT_KT / 4) * DSEG;
+  constexpr int VREG = (VPAIRS + AT_THREADS - 1) / AT_THREADS;
+  bf16x8 kr[KREG], vr[VREG][4];
+  auto load_tile = [&](const Tile& tl) {
 #pragma unroll
-    for (int i = 0; i < (AT_KT * DSEG) / AT_THREADS; ++i) {
+    for (int i = 0; i < KREG; ++i) {
       const int seg = tid + AT_THREADS * i;
-      const int kr = seg / DSEG;
-      const int ds = seg - kr * DSEG;
-      bf16x8 val = zero_bf16x8();
-      if (kr < nvalid) val = load_bf16x8(ksrc + ((size_t)(key_row0 + kr) * p.Hkv + hk) * D + ds * 8);
-      *reinterpret_cast<bf16x8*>(&k_s[kr * KSTR + ds * 8]) = val;
+      const int krow = seg / DSEG;
+      const int ds = seg - krow * DSEG;
+      kr[i] = load_bf16x8(tl.k + (size_t)min(krow, tl.nvalid - 1) * p.Hkv * D + ds * 8);
     }
-    // V tile -> LDS, transposed ([d][key], permuted key order).
-    for (int pr = tid; pr < (AT_KT / 4) * DSEG; pr += AT_THREADS) {
+#pragma unroll
+    for (int i = 0; i < VREG; ++i) {
+      const int pr = min(tid + AT_THREADS * i, VPAIRS - 1);
       const int k4 = pr / DSEG;
       const int ds = pr - k4 * DSEG;
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4)
+        vr[i][c4] = load_bf16x8(tl.v + (size_t)min(4 * k4 + c4, tl.nvalid - 1) * p.Hkv * D + ds * 8);
+    }
+  };
+  // Rows past nvalid are zeroed here (not right after the loads, which
+  // would stall on them); their scores are masked to -inf anyway.
+  auto store_tile = [&](int nvalid) {
+#pragma unroll
+    for (int i = 0; i < KREG; ++i) {
+      const int seg = tid + AT_THREADS * i;
+      const int krow = seg / DSEG;
+      const int ds = seg - krow * DSEG;
+      *reinterpret_cast<bf16x8*>(&k_s[krow * KSTR + ds * 8]) = krow < nvalid ? kr[i] : zero_bf16x8();
+    }
+#pragma unroll
+    for (int i = 0; i < VREG; ++i) {
+      const int pr = tid + AT_THREADS * i;
+      if (pr >= VPAIRS) break;
+      const int k4 = pr / DSEG;
+      const int ds = pr - k4 * DSEG;
+      const int pos = vt_pos4(k4);
       bf16x8 v4[4];
 #pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) {
-        const int kr = 4 * k4 + c4;
-        v4[c4] = (kr < nvalid)
-                     ? load_bf16x8(vsrc + ((size_t)(key_row0 + kr) * p.Hkv + hk) * D + ds * 8)
-                     : zero_bf16x8();
-      }
-      const int pos = vt_pos4(k4);
+      for (int c4 = 0; c4 < 4; ++c4) v4[c4] = (4 * k4 + c4 < nvalid) ? vr[i][c4] : zero_bf16x8();
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         bf16x4 col;
@@ -182,70 +220,82 @@ __global__ __launch_bounds__(AT_THREADS) void lane_attn_kernel(AttnParams p) {
         *reinterpret_cast<bf16x4*>(&vt_s[(ds * 8 + e) * VSTR + pos]) = col;
       }
     }
+  };
+
+  int kt = kt0;
+  Tile cur = tile_at(kt);
+  kt = next_kt(kt);
+  if (cur.nvalid) load_tile(cur);
+  while (cur.nvalid) {
+    __syncthreads();  // the previous tile is no longer read
+    store_tile(cur.nvalid);
     __syncthreads();
-    if (!vis_w) continue;
-
-    const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
-    f32x16 sacc[2];
+    // Prefetch the next visible tile while this one is multiplied.
+    const Tile nxt = tile_at(kt);
+    kt = next_kt(kt);
+    if (nxt.nvalid) load_tile(nxt);
+    if (cur.vis) {
+      const int nvalid = cur.nvalid;
+      const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
+      f32x16 sacc[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-      if (kb < nsub) {
+        for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+        if (kb < nsub) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
-          sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
+          for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
+            sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
+          }
+        }
+      }
+      // Scale into log2 units, mask invalid keys, online softmax update.
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float x = (key < nvalid) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
+          sacc[kb][r] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, xor32(mx));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = exp2_fast(m_run - m_new);
+      // P in bf16 (round-to-nearest-even), packed per 16-key MFMA step;
+      // the row sum uses the rounded values so O is a convex combination.
+      float rs = 0.f;
+      bf16x8 pk[4];
+#pragma unroll
+      for (int ks2 = 0; ks2 < 4; ++ks2)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint16_t bits = f32_to_bf16_bits(exp2_fast(sacc[ks2 >> 1][8 * (ks2 & 1) + e] - m_new));
+          pk[ks2][e] = __builtin_bit_cast(__bf16, bits);
+          rs += bf16_bits_to_f32(bits);
+        }
+      rs += xor32(rs);
+      l_run = l_run * alpha + rs;
+      m_run = m_new;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+      // O^T += V^T P^T, one 16-key MFMA step at a time.
+#pragma unroll
+      for (int ks2 = 0; ks2 < 4; ++ks2) {
+        if ((ks2 >> 1) < nsub) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(&vt_s[(dt * 32 + r32) * VSTR + ks2 * 16 + hh * 8]);
+            oacc[dt] = mfma32x32x16(a, pk[ks2], oacc[dt]);
+          }
         }
       }
     }
-    // Scale into log2 units, mask invalid keys, online softmax update.
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        const float x = (key < nvalid) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
-        sacc[kb][r] = x;
-        mx = fmaxf(mx, x);
-      }
-    mx = fmaxf(mx, xor32(mx));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2_fast(m_run - m_new);
-    float rs = 0.f;
-    uint16_t pb[2][16];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const uint16_t b = f32_to_bf16_bits(exp2_fast(sacc[kb][r] - m_new));
-        pb[kb][r] = b;
-        rs += bf16_bits_to_f32(b);
-      }
-    rs += xor32(rs);
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
-
-    // O^T += V^T P^T, one 16-key MFMA step at a time.
-#pragma unroll
-    for (int ks2 = 0; ks2 < 4; ++ks2) {
-      if ((ks2 >> 1) < nsub) {
-        uint16_t bb[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) bb[e] = pb[ks2 >> 1][8 * (ks2 & 1) + e];
-        const bf16x8 pbv = __builtin_bit_cast(bf16x8, bb);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&vt_s[(dt * 32 + r32) * VSTR + ks2 * 16 + hh * 8]);
-          oacc[dt] = mfma32x32x16(a, pbv, oacc[dt]);
-        }
-      }
-    }
+    cur = nxt;
   }
 
   if (!active || r32 >= nrows) return;
@@ -330,9 +380,9 @@ __global__ __launch_bounds__(256) void prefix_scatter_kernel(const int32_t* idx,
 // ------------------------------------------------------------------ host
 static int choose_split(int base_wgs, int total_key_tiles) {
   // Short grids leave most of the 256 CUs idle: split the key tiles (each
-  // split keeps at least two tiles) until about 256 workgroups exist.
+  // split keeps at least one tile) until about 256 workgroups exist.
   int s = 1;
-  while (s < 4 && base_wgs * s < 256 && total_key_tiles / (2 * s) >= 2) s *= 2;
+  while (s < 8 && base_wgs * s < 256 && 2 * s <= total_key_tiles) s *= 2;
   return s;
 }
 

@@ -259,27 +259,46 @@ void lmhead_partial_kernel(LmParams p) {
   }
 }
 
-// One wavefront per scored row: lanes merge strided runs of vocab-tile
-// partials in ascending order, then a fixed xor-butterfly combines lanes.
-__global__ __launch_bounds__(256) void lmhead_merge_kernel(const LmPartial* part, int N, int n_vt,
-                                                           int nt_cols, float* conf, int32_t* argmax,
-                                                           float* lse) {
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (n >= N) return;
+// One 256-thread workgroup per scored row.  Thread t merges vocab-tile
+// partials t, t+256, ... in ascending order (loads issued four at a time so
+// they overlap), then a fixed xor butterfly combines the lanes of each
+// wavefront and wavefront 0 combines the four wavefront results in order.
+constexpr int LM_MERGE_THREADS = 256;
+__global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
+    const LmPartial* part, int N, int n_vt, int nt_cols, float* conf, int32_t* argmax, float* lse) {
+  __shared__ float sm[LM_MERGE_THREADS / kWave], ss[LM_MERGE_THREADS / kWave];
+  __shared__ int si[LM_MERGE_THREADS / kWave];
+  const int n = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
   const int nt = n / nt_cols;
   const int col = n - nt * nt_cols;
   const LmPartial* base = part + (size_t)nt * n_vt * nt_cols + col;
   float m = -INFINITY, s = 0.f;
   int idx = 0x7fffffff;
-  for (int v = lane; v < n_vt; v += kWave) {
-    const LmPartial q = base[(size_t)v * nt_cols];
-    merge_state(m, s, idx, q.m, q.s, q.idx);
+  for (int v0 = tid; v0 < n_vt; v0 += 4 * LM_MERGE_THREADS) {
+    LmPartial q[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int v = v0 + j * LM_MERGE_THREADS;
+      q[j] = base[(size_t)min(v, n_vt - 1) * nt_cols];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (v0 + j * LM_MERGE_THREADS < n_vt) merge_state(m, s, idx, q[j].m, q[j].s, q[j].idx);
   }
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1)
     merge_state(m, s, idx, __shfl_xor(m, o, kWave), __shfl_xor(s, o, kWave), __shfl_xor(idx, o, kWave));
   if (lane == 0) {
+    sm[w] = m;
+    ss[w] = s;
+    si[w] = idx;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int ww = 1; ww < LM_MERGE_THREADS / kWave; ++ww) merge_state(m, s, idx, sm[ww], ss[ww], si[ww]);
     conf[n] = 1.0f / s;
     argmax[n] = idx;
     if (lse) lse[n] = m + logf(s);
@@ -359,7 +378,7 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
       AL_LM_CASE(8)
   }
 #undef AL_LM_CASE
-  hipLaunchKernelGGL(lmhead_merge_kernel, dim3((N + 3) / 4), dim3(256), 0, stream, p.part, N,
+  hipLaunchKernelGGL(lmhead_merge_kernel, dim3(N), dim3(LM_MERGE_THREADS), 0, stream, p.part, N,
                      L.n_vt, L.nt_cols, conf, argmax, lse);
   return hipGetLastError();
 }
