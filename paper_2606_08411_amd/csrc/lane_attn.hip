@@ -183,8 +183,8 @@ __global__ __launch_bounds__(AT_THREADS) void lane_attn_kernel(AttnParams p) {
 #pragma unroll
     for (int i = 0; i < VREG; ++i) {
       const int pr = min(tid + AT_THREADS * i, VPAIRS - 1);
-      const int k4 = pr / DSEG;
-      const int ds = pr - k4 * DSEG;
+      const int k4 = pr % (AT_KT / 4);
+      const int ds = pr / (AT_KT / 4);
 #pragma unroll
       for (int c4 = 0; c4 < 4; ++c4)
         vr[i][c4] = load_bf16x8(tl.v + (size_t)min(4 * k4 + c4, tl.nvalid - 1) * p.Hkv * D + ds * 8);
@@ -204,8 +204,10 @@ __global__ __launch_bounds__(AT_THREADS) void lane_attn_kernel(AttnParams p) {
     for (int i = 0; i < VREG; ++i) {
       const int pr = tid + AT_THREADS * i;
       if (pr >= VPAIRS) break;
-      const int k4 = pr / DSEG;
-      const int ds = pr - k4 * DSEG;
+      // Key group fastest across threads: the transposed 8-byte stores of a
+      // wavefront then hit distinct banks (d-segment fastest conflicts 16x).
+      const int k4 = pr % (AT_KT / 4);
+      const int ds = pr / (AT_KT / 4);
       const int pos = vt_pos4(k4);
       bf16x8 v4[4];
 #pragma unroll

@@ -12,10 +12,9 @@
 // shaped for HBM streaming rather than for MFMA reuse (measured on MI355X):
 // * each wavefront owns 16 vocabulary rows (the A operand of the 16x16x32
 //   bf16 MFMA); per chunk it loads 256 contiguous bytes of each row
-//   (4 lanes x 64 B, issued back to back) straight into registers, one
-//   chunk ahead of the MFMAs -- each W element is used by one wavefront;
-// * the K index inside a chunk is permuted identically on W and H so each
-//   lane's 128 B run maps onto consecutive MFMA k-steps;
+//   (4 instructions x 4 lanes x 16 B, issued back to back) straight into
+//   registers, two chunks ahead of the MFMAs -- each W element is used by
+//   one wavefront only;
 // * the chunk of the scored hidden rows (B operand, <= 128 rows) is staged
 //   once per workgroup in LDS and shared by its wavefronts; the LDS buffer
 //   is small enough for several workgroups per CU, which keeps enough W
@@ -48,7 +47,7 @@ struct LmParams {
   const int32_t* row_idx;
   const uint16_t* W;
   const uint8_t* sup;
-  LmPartial* part;  // [n_nt][n_vt][nt_cols]
+  LmPartial* part;  // [n_nt][nt_cols][n_vt]: a row's partials are contiguous
   int N, d, V, eos_id;
   int n_vt, n_nt, nt_cols, tiles_total, tiles_per_xcd;
 };
@@ -70,22 +69,28 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
   m = M;
 }
 
-// WAVES wavefronts x 16 vocab rows per workgroup; KC hidden elements per
-// chunk (each lane streams KC/4 contiguous elements of its row per chunk).
+// WAVES wavefronts x 16 vocab rows per workgroup.  W is streamed in chunks
+// of KC hidden elements (each lane loads KC/4 contiguous elements of its row
+// per chunk, PF chunks ahead of the MFMAs, so the MFMA work overlaps the
+// stream).  The hidden chunk is staged once per workgroup in LDS.
 // OCC: wavefronts per SIMD the register allocation must allow.
-template <int NFRAG, bool RAGGED, int WAVES, int KC, int OCC>
+template <int NFRAG, bool RAGGED, int WAVES, int KC, int PF, int OCC>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 void lmhead_partial_kernel(LmParams p) {
   constexpr int THREADS = WAVES * 64;
   constexpr int VT = 16 * WAVES;                 // vocab rows per workgroup
-  constexpr int LANE_K = KC / 4;                 // contiguous K per lane per chunk
-  constexpr int STEPS = LANE_K / 8;              // MFMA k-steps per chunk
+  constexpr int STEPS = KC / 32;                 // MFMA k-steps per chunk
+  constexpr int KCH = KC;                        // hidden elements staged at once
   constexpr int NT = 16 * NFRAG;                 // scored rows (columns) per tile
-  constexpr int KSEG = KC / 8;                   // 16-byte segments per staged row
-  constexpr int STRIDE = KC + 8;                 // bf16 per staged row (+16 B pad)
-  constexpr int RPP = THREADS / KSEG;            // staged rows per pass
-  constexpr int HREG = (NT + RPP - 1) / RPP;
-  constexpr int ROWS_STAGED = HREG * RPP;        // >= NT; extra rows unused
+  constexpr int KSEG = KCH / 8;                  // 16-byte segments per staged row
+  // bf16 per staged row: +32 B of padding makes the B-operand reads below
+  // conflict-free (measured on gfx950; +16 B costs 2x in bank conflicts).
+  constexpr int STRIDE = KCH + 16;
+  constexpr int SEGS = NT * KSEG;
+  constexpr int HREG = (SEGS + THREADS - 1) / THREADS;
+  // Rows past NT are written (by the last staging pass) but never read:
+  // every thread stores, so the staging code has no divergent branch.
+  constexpr int ROWS_STAGED = HREG * THREADS / KSEG;
   __shared__ __attribute__((aligned(16))) uint16_t hs[ROWS_STAGED * STRIDE];
   // After the K loop the staging buffer holds the per-wavefront (m, s, idx).
   static_assert(sizeof(hs) >= 3 * sizeof(float) * WAVES * NT, "reduction scratch");
@@ -113,20 +118,26 @@ void lmhead_partial_kernel(LmParams p) {
   // not post-processed after loading.  A W segment past d meets hidden
   // values zeroed at the LDS store; rows past V are dropped in the epilogue.
   const uint16_t* wrow = p.W + (size_t)min(v0 + r16, p.V - 1) * d;
-  const uint16_t* wlane = wrow + g4 * LANE_K;
-  const int hk = (tid % KSEG) * 8;
-  // Row offsets into `hidden` (32-bit: n_rows * d < 2^31 is checked).
-  unsigned hrow[HREG];
+  const uint16_t* wlane = wrow + g4 * 8;
+  // Hidden staging: thread tid moves segments tid + THREADS*i of the
+  // NT x KSEG staged block (row-major); 32-bit row offsets (n_rows * d <
+  // 2^31 is checked by the caller).
+  unsigned hoff[HREG];
+  int hcol[HREG];
+  int hdst[HREG];
   unsigned hvalid = 0;
 #pragma unroll
   for (int i = 0; i < HREG; ++i) {
-    const int row = tid / KSEG + RPP * i;
+    const int seg = tid + THREADS * i;
+    const int row = seg / KSEG;
+    const int k = (seg - row * KSEG) * 8;
     const bool ok = row < ncols;
     const int n = n0 + (ok ? row : 0);
-    hrow[i] = (unsigned)(p.row_idx ? p.row_idx[n] : n) * (unsigned)d + (unsigned)hk;
+    hoff[i] = (unsigned)(p.row_idx ? p.row_idx[n] : n) * (unsigned)d + (unsigned)k;
+    hcol[i] = k;
+    hdst[i] = row * STRIDE + k;
     hvalid |= (ok ? 1u : 0u) << i;
   }
-  const int hdst0 = (tid / KSEG) * STRIDE + hk;
 
   f32x4 acc[NFRAG];
 #pragma unroll
@@ -134,79 +145,96 @@ void lmhead_partial_kernel(LmParams p) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[f][r] = 0.f;
 
-  bf16x8 wa[STEPS], wb[STEPS], hr[HREG];
+  bf16x8 wr[PF + 1][STEPS], hr[HREG];
+  // Step s of a chunk covers K elements kc + s*32 .. +32; lane group g4
+  // takes kc + s*32 + g4*8 .. +8 on both operands, so each W load
+  // instruction reads 64 contiguous bytes of every row of the wavefront.
   auto load_w = [&](bf16x8* wv, int kc) {
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
       if (RAGGED) {
-        const int k = kc + g4 * LANE_K + s * 8;
+        const int k = kc + s * 32 + g4 * 8;
         wv[s] = load_bf16x8(wrow + (k < d ? k : 0));
       } else {
-        wv[s] = load_bf16x8(wlane + kc + s * 8);
+        wv[s] = load_bf16x8(wlane + kc + s * 32);
       }
     }
   };
-  auto load_h = [&](int kc) {
-    const bool kin = !RAGGED || kc + hk < d;
+  // Hidden segment i of the block starting at kh covers element
+  // hcol[i] + kh of its row; past d it reads the row start instead and is
+  // zeroed at the LDS store.
+  auto load_h = [&](int kh) {
 #pragma unroll
-    for (int i = 0; i < HREG; ++i) hr[i] = load_bf16x8(p.hidden + (hrow[i] + (kin ? kc : -hk)));
+    for (int i = 0; i < HREG; ++i) {
+      if (RAGGED)
+        hr[i] = load_bf16x8(p.hidden + (hcol[i] + kh < d ? hoff[i] + kh : hoff[i] - hcol[i]));
+      else
+        hr[i] = load_bf16x8(p.hidden + (hoff[i] + kh));
+    }
   };
   // Zeroing past d and for unused columns happens at the LDS store, where
   // the data is awaited anyway (a select right after a load would stall).
-  auto store_h = [&](int kc) {
-    const bool kin = !RAGGED || kc + hk < d;
+  auto store_h = [&](int kh) {
 #pragma unroll
-    for (int i = 0; i < HREG; ++i)
-      *reinterpret_cast<bf16x8*>(&hs[hdst0 + RPP * i * STRIDE]) =
-          (kin && ((hvalid >> i) & 1u)) ? hr[i] : zero_bf16x8();
+    for (int i = 0; i < HREG; ++i) {
+      const bool kin = !RAGGED || hcol[i] + kh < d;
+      *reinterpret_cast<bf16x8*>(&hs[hdst[i]]) = (kin && ((hvalid >> i) & 1u)) ? hr[i] : zero_bf16x8();
+    }
   };
   // MFMA step s covers, for lane group g4, the K elements
-  // kc + g4*LANE_K + s*8 + e (e = 0..7) on both operands.
+  // kc + s*32 + g4*8 + e (e = 0..7) on both operands.
   auto mma = [&](const bf16x8* wv) {
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
 #pragma unroll
       for (int f = 0; f < NFRAG; ++f) {
-        const bf16x8 bv =
-            *reinterpret_cast<const bf16x8*>(&hs[(f * 16 + r16) * STRIDE + g4 * LANE_K + s * 8]);
+        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(
+            &hs[(f * 16 + r16) * STRIDE + s * 32 + g4 * 8]);
         acc[f] = mfma16x16x32(wv[s], bv, acc[f]);
       }
     }
   };
-  // One chunk whose successor exists: load the next hidden chunk, then
-  // prefetch W(next) -- in that order, because the LDS store waits for the
-  // hidden loads and the load counter is in-order -- multiply, restage LDS.
-  auto step = [&](const bf16x8* cur, bf16x8* nxt, int kc_next) {
-    load_h(kc_next);
-    load_w(nxt, kc_next);
-    // Keep the prefetch loads ahead of the MFMAs (the scheduler would
-    // otherwise sink them and shorten the prefetch distance).
+
+  // Chunk c uses register buffer c % (PF+1); W(c+PF) is prefetched while
+  // chunk c is multiplied.  The next hidden chunk's loads are issued before
+  // that prefetch (the load counter is in-order and the LDS store waits for
+  // them).  The steady-state loop has every prefetch in range and no
+  // branches; the last chunks are peeled.
+  const int nch = (d + KC - 1) / KC;
+  load_h(0);
+#pragma unroll
+  for (int j = 0; j < PF; ++j)
+    if (j < nch) load_w(wr[j], j * KC);
+  store_h(0);
+  __syncthreads();
+  auto chunk_full = [&](int c, const bf16x8* cur, bf16x8* pre) {
+    load_h((c + 1) * KC);
+    load_w(pre, (c + PF) * KC);
     __builtin_amdgcn_sched_barrier(0);
     mma(cur);
     __syncthreads();  // every wavefront is done with this hidden chunk
-    store_h(kc_next);
+    store_h((c + 1) * KC);
     __syncthreads();
   };
-
-  // W chunk c+1 is in flight while chunk c is multiplied; registers
-  // ping-pong between wa (even chunks) and wb (odd chunks) without copies.
-  // The steady-state loop has no tail conditions; the last chunk is peeled.
-  const int nch = (d + KC - 1) / KC;
-  load_h(0);
-  load_w(wa, 0);
-  store_h(0);
-  __syncthreads();
+  auto chunk_tail = [&](int c, const bf16x8* cur, bf16x8* pre) {
+    const bool has_next = c + 1 < nch;
+    if (has_next) load_h((c + 1) * KC);
+    if (c + PF < nch) load_w(pre, (c + PF) * KC);
+    mma(cur);
+    if (has_next) {
+      __syncthreads();
+      store_h((c + 1) * KC);
+      __syncthreads();
+    }
+  };
   int c = 0;
-  for (; c + 2 < nch; c += 2) {
-    step(wa, wb, (c + 1) * KC);
-    step(wb, wa, (c + 2) * KC);
+  for (; c + 2 * PF < nch; c += PF + 1) {
+#pragma unroll
+    for (int j = 0; j <= PF; ++j) chunk_full(c + j, wr[j], wr[(j + PF) % (PF + 1)]);
   }
-  if (c + 1 < nch) {
-    step(wa, wb, (c + 1) * KC);
-    mma(wb);
-  } else {
-    mma(wa);
-  }
+#pragma unroll
+  for (int j = 0; j < 2 * PF + 1; ++j)
+    if (c + j < nch) chunk_tail(c + j, wr[j % (PF + 1)], wr[(j + PF) % (PF + 1)]);
   __syncthreads();
 
   // Epilogue: lane (r16, g4) holds vocab rows v0 + 4*g4 + r (r = 0..3) of
@@ -255,7 +283,7 @@ void lmhead_partial_kernel(LmParams p) {
     q.s = s;
     q.idx = idx;
     q.pad = 0;
-    p.part[((size_t)nt * p.n_vt + vt) * p.nt_cols + col] = q;
+    p.part[((size_t)nt * p.nt_cols + col) * p.n_vt + vt] = q;
   }
 }
 
@@ -274,7 +302,7 @@ __global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
   const int w = tid >> 6;
   const int nt = n / nt_cols;
   const int col = n - nt * nt_cols;
-  const LmPartial* base = part + (size_t)nt * n_vt * nt_cols + col;
+  const LmPartial* base = part + ((size_t)nt * nt_cols + col) * n_vt;
   float m = -INFINITY, s = 0.f;
   int idx = 0x7fffffff;
   for (int v0 = tid; v0 < n_vt; v0 += 4 * LM_MERGE_THREADS) {
@@ -282,7 +310,7 @@ __global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int v = v0 + j * LM_MERGE_THREADS;
-      q[j] = base[(size_t)min(v, n_vt - 1) * nt_cols];
+      q[j] = base[min(v, n_vt - 1)];
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -308,6 +336,9 @@ __global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
 // ------------------------------------------------------------------ host
 constexpr int LM_WAVES = 8;
 constexpr int LM_KC = 128;
+// Prefetch depth: two W chunks in flight where registers allow (up to 96
+// scored columns), one beyond that (no spills at 128 columns).
+constexpr int lm_pf(int nfrag) { return nfrag <= 6 ? 2 : 1; }
 constexpr int LM_OCC = 4;
 constexpr int LM_VT = 16 * LM_WAVES;
 
@@ -360,10 +391,10 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, LM_OCC>), grid, block, 0,  \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), LM_OCC>), grid, block, 0,  \
                          stream, p);                                                          \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, LM_OCC>), grid, block, 0, \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), LM_OCC>), grid, block, 0, \
                          stream, p);                                                          \
     break;
   switch (L.nfrag) {
