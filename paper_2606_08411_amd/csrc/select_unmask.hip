@@ -8,10 +8,11 @@
 // valid prefix length ("Advancement control") are read on the updated state.
 //
 // The whole step touches a few KB, so it is latency-bound: one workgroup
-// keeps the lane state in LDS, ranks top-k candidates by comparison counting
-// (ties: lower position first), compacts the unmasked / still-masked row
-// lists in order with wavefront ballots, and reduces each lane's statistics
-// with wavefront shuffles.
+// reads every input once into LDS (one memory latency instead of one per
+// phase or per loop iteration), ranks top-k candidates by comparison
+// counting (ties: lower position first), compacts the unmasked /
+// still-masked row lists in order with wavefront ballots, and reduces each
+// lane's statistics with wavefront shuffles.
 #include "common.h"
 #include "launch.h"
 
@@ -55,7 +56,11 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   __shared__ int s_tok[kSelMaxPositions];
   __shared__ uint8_t s_msk[kSelMaxPositions];
   __shared__ uint8_t s_sel[kSelMaxPositions];  // bit0 selected, bit1 candidate
+  __shared__ int s_pos[kSelMaxPositions];      // row_pos
+  __shared__ float s_conf[kSelMaxPositions];
+  __shared__ int s_arg[kSelMaxPositions];
   __shared__ int s_lo[kSelMaxLanes], s_hi[kSelMaxLanes], s_cnt[kSelMaxLanes], s_nsel[kSelMaxLanes];
+  __shared__ int s_blen[kSelMaxLanes], s_k[kSelMaxLanes];
   __shared__ int s_wu[SEL_WAVES], s_ws[SEL_WAVES];
 
   const SelHost& h = p.h;
@@ -68,25 +73,32 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     s_tok[i] = p.tokens[i];
     s_msk[i] = p.is_masked[i];
   }
+  for (int n = tid; n < N; n += SEL_THREADS) {
+    s_pos[n] = p.row_pos[n];
+    s_conf[n] = p.conf[n];
+    s_arg[n] = p.argmax[n];
+  }
   if (tid < kSelMaxLanes) {
     s_lo[tid] = 0;
     s_hi[tid] = 0;
     s_cnt[tid] = 0;
     s_nsel[tid] = 0;
+    s_blen[tid] = tid < L ? h.b_len[tid] : 0;
+    s_k[tid] = tid < L ? h.k_lane[tid] : 0;
   }
   __syncthreads();
 
   // Candidates, lane row ranges (row_pos is ascending, so each lane's rows
   // are contiguous) and threshold passes.
   for (int n = tid; n < N; n += SEL_THREADS) {
-    const int pos = p.row_pos[n];
+    const int pos = s_pos[n];
     const int ln = pos / B;
     const int i = pos - ln * B;
-    if (n == 0 || p.row_pos[n - 1] / B != ln) s_lo[ln] = n;
-    if (n == N - 1 || p.row_pos[n + 1] / B != ln) s_hi[ln] = n + 1;
-    const bool cand = i < h.b_len[ln] && s_msk[pos];
+    if (n == 0 || s_pos[n - 1] / B != ln) s_lo[ln] = n;
+    if (n == N - 1 || s_pos[n + 1] / B != ln) s_hi[ln] = n + 1;
+    const bool cand = i < s_blen[ln] && s_msk[pos];
     uint8_t f = cand ? 2 : 0;
-    if (h.mode == 0 && cand && p.conf[n] >= h.tau) {
+    if (h.mode == 0 && cand && s_conf[n] >= h.tau) {
       f |= 1;
       atomicAdd(&s_cnt[ln], 1);
     }
@@ -98,16 +110,16 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   // a candidate is chosen when fewer than k candidates of its lane beat it.
   for (int n = tid; n < N; n += SEL_THREADS) {
     if (!(s_sel[n] & 2)) continue;
-    const int pos = p.row_pos[n];
+    const int pos = s_pos[n];
     const int ln = pos / B;
-    const int k = (h.mode == 1) ? h.k_lane[ln] : (s_cnt[ln] == 0 ? h.fallback_k : 0);
+    const int k = (h.mode == 1) ? s_k[ln] : (s_cnt[ln] == 0 ? h.fallback_k : 0);
     if (k <= 0) continue;
-    const float c = p.conf[n];
+    const float c = s_conf[n];
     int rank = 0;
     for (int m = s_lo[ln]; m < s_hi[ln]; ++m) {
       if (!(s_sel[m] & 2)) continue;
-      const float cm = p.conf[m];
-      rank += (cm > c) || (cm == c && p.row_pos[m] < pos);
+      const float cm = s_conf[m];
+      rank += (cm > c) || (cm == c && s_pos[m] < pos);
     }
     if (rank < k) s_sel[n] |= 1;
   }
@@ -118,8 +130,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     const int sel = s_sel[n] & 1;
     p.unmask_flag[n] = (uint8_t)sel;
     if (sel) {
-      const int pos = p.row_pos[n];
-      const int tok = p.argmax[n];
+      const int pos = s_pos[n];
+      const int tok = s_arg[n];
       p.tokens[pos] = tok;
       p.is_masked[pos] = 0;
       s_tok[pos] = tok;
@@ -134,7 +146,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   for (int b0 = 0; b0 < N; b0 += SEL_THREADS) {
     const int n = b0 + tid;
     const bool fu = n < N && (s_sel[n] & 1);
-    const bool fs = n < N && !fu && s_msk[p.row_pos[n]];
+    const bool fs = n < N && !fu && s_msk[s_pos[n]];
     const unsigned long long bu = __ballot(fu);
     const unsigned long long bs = __ballot(fs);
     const unsigned long long lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -152,8 +164,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
       tot_u += s_wu[ww];
       tot_s += s_ws[ww];
     }
-    if (fu) p.unmasked_pos[off_u + __popcll(bu & lt)] = p.row_pos[n];
-    if (fs) p.still_pos[off_s + __popcll(bs & lt)] = p.row_pos[n];
+    if (fu) p.unmasked_pos[off_u + __popcll(bu & lt)] = s_pos[n];
+    if (fs) p.still_pos[off_s + __popcll(bs & lt)] = s_pos[n];
     base_u += tot_u;
     base_s += tot_s;
     __syncthreads();
