@@ -29,6 +29,17 @@ i < b_len; delimiters and EOS as in Section 3.2):
               t_lane >= t_min (eq. fork_condition); the product is formed
               in fp32.
 * n_sel     = number of positions of the lane transferred by this call.
+* n_draft   = number of lookahead drafts written into the lane this call.
+
+Lookahead drafts (Section 3.2, "Advancement control", and eq. lane_input):
+the input of a generate lane is its state followed by an optional lookahead
+window; only the first b_len logits drive the transfer rule.  Here a lane
+block holds B positions, so the window is positions [b_len, B).  A masked
+window position of a generate lane whose confidence reaches tau_future and
+whose predicted token is not EOS takes that token as a draft (unmask_flag
+2; it becomes unmasked and is listed in unmasked_pos).  Refine lanes never
+draft.  tau_future None (or above 1, since conf <= 1) disables drafting.
+The paper gives no value for tau_future.
 
 Decisions that compare floating point values (threshold, ordering, fill
 ratio) are taken in fp32, the precision the device kernel uses.
@@ -40,14 +51,16 @@ ROLE_REF = 1
 MODE_THRESHOLD = 0
 MODE_TOPK = 1
 
-STAT_SPLIT, STAT_FILLED, STAT_VALID, STAT_FORK, STAT_NSEL = range(5)
+STAT_SPLIT, STAT_FILLED, STAT_VALID, STAT_FORK, STAT_NSEL, STAT_NDRAFT = range(6)
+N_STATS = 6
 
 
 def lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane, delim_ids,
                         eos_id, rho_min, t_min):
-    """Returns (lane_stats [L][5] int32, delim_flag [L*B] uint8)."""
+    """Returns (lane_stats [L][6] int32, delim_flag [L*B] uint8); the
+    n_sel and n_draft columns are left at zero here."""
     L = len(role)
-    stats = np.zeros((L, 5), dtype=np.int32)
+    stats = np.zeros((L, N_STATS), dtype=np.int32)
     dflag = np.zeros(L * B, dtype=np.uint8)
     dset = set(int(x) for x in delim_ids)
     for lane in range(L):
@@ -78,12 +91,13 @@ def lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane, delim_ids,
 
 def select_unmask(conf, argmax, row_pos, tokens, is_masked, B, role, b_len, t_lane,
                   mode, tau, fallback_k=0, k_lane=None, delim_ids=(0, 1), eos_id=2,
-                  rho_min=0.5, t_min=2):
+                  rho_min=0.5, t_min=2, tau_future=None):
     """Per-lane transfer on the rows row_pos (flat positions lane*B + i,
-    ascending) followed by the boundary statistics.
+    ascending), lookahead drafts, then the boundary statistics.
 
-    Returns dict(tokens, is_masked, unmask_flag [N] u8, unmasked_pos,
-    still_masked_pos, counts [2], lane_stats [L][5], delim_flag [L*B])."""
+    Returns dict(tokens, is_masked, unmask_flag [N] u8 (1 transfer,
+    2 draft), unmasked_pos, still_masked_pos, counts [2], lane_stats [L][6],
+    delim_flag [L*B])."""
     conf32 = np.asarray(conf, dtype=np.float32)
     tau32 = np.float32(tau)
     row_pos = np.asarray(row_pos, dtype=np.int64)
@@ -107,18 +121,28 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, B, role, b_len, t_la
             raise ValueError(mode)
         for n in chosen:
             flag[n] = 1
+    if tau_future is not None:
+        tf32 = np.float32(tau_future)
+        for n in range(N):
+            pos = int(row_pos[n])
+            lane, i = pos // B, pos % B
+            if (int(role[lane]) == ROLE_GEN and i >= int(b_len[lane]) and is_masked[pos]
+                    and conf32[n] >= tf32 and int(argmax[n]) != int(eos_id)):
+                flag[n] = 2
     for n in range(N):
         if flag[n]:
             tokens[row_pos[n]] = argmax[n]
             is_masked[row_pos[n]] = 0
-    unmasked_pos = row_pos[flag == 1].astype(np.int32)
+    unmasked_pos = row_pos[flag != 0].astype(np.int32)
     still = np.array([row_pos[n] for n in range(N) if not flag[n] and is_masked[row_pos[n]]],
                      dtype=np.int32)
     stats, dflag = lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane,
                                        delim_ids, eos_id, rho_min, t_min)
     for n in range(N):
-        if flag[n]:
+        if flag[n] == 1:
             stats[row_pos[n] // B, STAT_NSEL] += 1
+        elif flag[n] == 2:
+            stats[row_pos[n] // B, STAT_NDRAFT] += 1
     return dict(tokens=tokens, is_masked=is_masked, unmask_flag=flag,
                 unmasked_pos=unmasked_pos, still_masked_pos=still,
                 counts=np.array([len(unmasked_pos), len(still)], dtype=np.int32),

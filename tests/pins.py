@@ -551,5 +551,113 @@ def check_lane_stats_scan(sel):
             assert not dflag[lane * B + n:(lane + 1) * B].any()
 
 
+def _parse_lookahead_golden():
+    cases = []
+    with open(os.path.join(GOLDEN, "lookahead_cases.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            lhs, rhs = line.split("||")
+            roles, b_len, toks, rows, mode, tau, fb, k_lane, tauf = [x.strip() for x in lhs.split("|")]
+            flags, nsel, ndraft = [x.strip() for x in rhs.split("|")]
+            lanes = [t.split(",") for t in toks.split("/")]
+            B = len(lanes[0])
+            assert all(len(t) == B for t in lanes)
+            flat = [x for t in lanes for x in t]
+            rws = [r.split(":") for r in rows.split(",")]
+            cases.append(dict(
+                role=np.array([0 if r == "gen" else 1 for r in roles.split(",")], np.uint8),
+                b_len=np.array([int(x) for x in b_len.split(",")], np.int32), B=B,
+                tokens=np.array([-1 if x == "M" else int(x) for x in flat], np.int32),
+                masked=np.array([x == "M" for x in flat], np.uint8),
+                row_pos=np.array([int(r[0]) for r in rws], np.int64),
+                conf=np.array([float(r[1]) for r in rws], np.float32),
+                arg=np.array([int(r[2]) for r in rws], np.int32),
+                mode=0 if mode == "threshold" else 1, tau=float(tau), fb=int(fb),
+                k_lane=np.array([int(x) for x in k_lane.split(",")], np.int32),
+                tau_future=float(tauf),
+                flags=[int(x) for x in flags.split(",")],
+                nsel=[int(x) for x in nsel.split(",")],
+                ndraft=[int(x) for x in ndraft.split(",")]))
+    return cases
+
+
+def check_lookahead_golden(sel):
+    """Hand-worked transfers and lookahead drafts
+    (tests/golden/lookahead_cases.txt), with the write-back they imply."""
+    cases = _parse_lookahead_golden()
+    assert len(cases) >= 5
+    for c in cases:
+        L = len(c["role"])
+        out = sel.select_unmask(c["conf"], c["arg"], c["row_pos"], c["tokens"], c["masked"],
+                                c["B"], c["role"], c["b_len"], np.full(L, 3, np.int32),
+                                c["mode"], c["tau"], c["fb"], c["k_lane"], eos_id=2,
+                                tau_future=c["tau_future"])
+        assert list(out["unmask_flag"]) == c["flags"], (c, out["unmask_flag"])
+        assert list(out["lane_stats"][:, 4]) == c["nsel"]
+        assert list(out["lane_stats"][:, 5]) == c["ndraft"]
+        hit = [n for n, f in enumerate(c["flags"]) if f]
+        tk = c["tokens"].copy()
+        mk = c["masked"].copy()
+        for n in hit:
+            tk[c["row_pos"][n]] = c["arg"][n]
+            mk[c["row_pos"][n]] = 0
+        assert np.array_equal(out["tokens"], tk) and np.array_equal(out["is_masked"], mk)
+        assert list(out["unmasked_pos"]) == [int(c["row_pos"][n]) for n in hit]
+
+
+def check_lookahead_properties(sel):
+    """On random states: drafting off (None, or tau_future above 1 since
+    conf <= 1) is the plain call; drafting never changes the in-region
+    decision or the boundary statistics (they read [0, b_len) only);
+    drafts lie in generate-lane windows on masked, non-EOS rows; lowering
+    tau_future only adds drafts."""
+    rng = np.random.default_rng(23)
+    for trial in range(40):
+        L = int(rng.integers(1, 5))
+        B = int(rng.integers(2, 9))
+        LB = L * B
+        is_masked = (rng.random(LB) < 0.7).astype(np.uint8)
+        row_pos = np.flatnonzero(rng.random(LB) < 0.9)
+        N = len(row_pos)
+        conf = (rng.integers(0, 17, N) / 16).astype(np.float32)
+        arg = rng.integers(2, 9, N).astype(np.int32)     # id 2 (EOS) occurs
+        tokens = rng.integers(0, 9, LB).astype(np.int32)
+        b_len = rng.integers(0, B + 1, L).astype(np.int32)
+        role = rng.integers(0, 2, L).astype(np.uint8)
+        t_lane = rng.integers(0, 5, L).astype(np.int32)
+        mode = int(rng.integers(0, 2))
+        k_lane = rng.integers(0, B + 1, L).astype(np.int32)
+        args = (conf, arg, row_pos, tokens, is_masked, B, role, b_len, t_lane, mode, 0.75, 1, k_lane)
+        plain = sel.select_unmask(*args)
+        for off in (None, 1.5):
+            o = sel.select_unmask(*args, tau_future=off)
+            for key in plain:
+                assert np.array_equal(o[key], plain[key]), (trial, key)
+        prev = None
+        for tf in (1.0, 0.75, 0.5, 0.0):
+            o = sel.select_unmask(*args, tau_future=tf)
+            f = o["unmask_flag"]
+            assert np.array_equal(f == 1, plain["unmask_flag"] == 1)
+            assert np.array_equal(o["lane_stats"][:, :5], plain["lane_stats"][:, :5])
+            assert np.array_equal(o["delim_flag"], plain["delim_flag"])
+            for n in np.flatnonzero(f == 2):
+                pos = int(row_pos[n])
+                assert role[pos // B] == 0 and pos % B >= b_len[pos // B]
+                assert is_masked[pos] and arg[n] != 2 and conf[n] >= np.float32(tf)
+            d = set(np.flatnonzero(f == 2).tolist())
+            if prev is not None:
+                assert prev <= d
+            prev = d
+        # tau_future = 0: every masked window row of a generate lane that
+        # does not predict EOS is drafted.
+        want = {n for n in range(N) if role[row_pos[n] // B] == 0
+                and row_pos[n] % B >= b_len[row_pos[n] // B]
+                and is_masked[row_pos[n]] and arg[n] != 2}
+        assert prev == want
+
+
 SELECT_CHECKS = [check_select_brute_force, check_select_threshold_extremes,
-                 check_lane_stats_golden, check_lane_stats_scan]
+                 check_lane_stats_golden, check_lane_stats_scan,
+                 check_lookahead_golden, check_lookahead_properties]

@@ -66,6 +66,16 @@ MUTANTS = {
         ("step condition ignored", "and int(t_lane[lane]) >= int(t_min))", ")"),
         ("top-k takes k+1", "chosen = order[:max(0, min(int(k_lane[lane]), len(cand)))]",
          "chosen = order[:max(0, min(int(k_lane[lane]) + 1, len(cand)))]"),
+        ("refine lanes draft", "if (int(role[lane]) == ROLE_GEN and i >= int(b_len[lane])",
+         "if (True and i >= int(b_len[lane])"),
+        ("window starts after b_len", "and i >= int(b_len[lane]) and is_masked[pos]",
+         "and i > int(b_len[lane]) and is_masked[pos]"),
+        ("strict draft threshold", "and conf32[n] >= tf32 and", "and conf32[n] > tf32 and"),
+        ("EOS drafted", "and int(argmax[n]) != int(eos_id)):", "):"),
+        ("unmasked window rows drafted", "and is_masked[pos]\n                    and conf32", "\n                    and conf32"),
+        ("drafts counted as transfers", "elif flag[n] == 2:\n            stats[row_pos[n] // B, STAT_NDRAFT] += 1",
+         "elif flag[n] == 2:\n            stats[row_pos[n] // B, STAT_NSEL] += 1"),
+        ("drafts left out of unmasked_pos", "unmasked_pos = row_pos[flag != 0]", "unmasked_pos = row_pos[flag == 1]"),
     ],
 }
 
