@@ -14,8 +14,9 @@
  *   lmhead_confidence   fused hidden->vocab GEMM + online softmax: per masked
  *                       position the max probability and its token id,
  *                       without writing the logits
- *   select_unmask       per-lane threshold / top-k transfer, write-back,
- *                       ordered compaction and boundary statistics
+ *   select_unmask       per-lane threshold / top-k transfer, lookahead
+ *                       drafts, write-back, ordered compaction and
+ *                       boundary statistics
  *
  * Conventions shared by every call
  * --------------------------------
@@ -78,7 +79,8 @@ typedef uint16_t al_bf16;
                              (float)filled >= rho_min * (float)b_len (fp32) and
                              t_lane >= t_min (eq. fork_condition)                  */
 #define AL_STAT_NSEL 4    /* positions of this lane transferred by this call      */
-#define AL_LANE_STATS 5
+#define AL_STAT_NDRAFT 5  /* lookahead drafts written into this lane by this call */
+#define AL_LANE_STATS 6
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char* al_status_string(int status);
@@ -174,7 +176,8 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * select_unmask -- per-lane transfer, write-back and boundary statistics.
+ * select_unmask -- per-lane transfer, lookahead drafts, write-back and
+ * boundary statistics.
  *
  * Defined by Section 3.2: the transfer rule is applied to each lane's valid
  * update region [0, b_len[l]) (refine lanes: the discovered prefix); the
@@ -182,6 +185,12 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
  * the lane's split point (eq. split_point, ValidBoundary taken as true),
  * fill ratio and step condition (eq. fork_condition) and valid prefix length
  * ("Advancement control") are computed on the updated state.
+ *
+ * Lookahead drafts ("Advancement control", eq. lane_input): positions
+ * [b_len[l], B) of a generate lane are its lookahead window.  A masked
+ * window row with conf >= tau_future (fp32) whose argmax is not eos_id is
+ * written back as a draft.  Refine lanes never draft.  Drafting is off
+ * when tau_future > 1 (conf never exceeds 1), e.g. +inf.
  *
  * Row n describes flat position row_pos[n] = lane*B + i.  A row is a
  * candidate of lane l = row_pos[n]/B when i < b_len[l] and the position is
@@ -203,8 +212,10 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
  * delim_ids host [n_delim] token ids, 0 <= n_delim <= AL_MAX_DELIMS
  * eos_id   token id ending the valid prefix (-1 = none)
  * rho_min, t_min  fork condition parameters
- * unmask_flag dev [N] uint8 out: 1 iff row n was transferred
- * unmasked_pos dev [N] int32 out: transferred positions, ascending
+ * tau_future fp32 (not NaN): lookahead draft threshold, > 1 = off
+ * unmask_flag dev [N] uint8 out: 1 row n was transferred, 2 drafted, else 0
+ * unmasked_pos dev [N] int32 out: transferred and drafted positions,
+ *          ascending
  * still_masked_pos dev [N] int32 out: positions of rows still masked,
  *          ascending (the next step's row list)
  * counts   dev [2] int32 out: {#unmasked_pos, #still_masked_pos}
@@ -217,7 +228,7 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
                   const uint8_t* role, const int32_t* b_len, const int32_t* t_lane,
                   int mode, float tau, int fallback_k, const int32_t* k_lane,
                   const int32_t* delim_ids, int n_delim, int eos_id,
-                  float rho_min, int t_min,
+                  float rho_min, int t_min, float tau_future,
                   uint8_t* unmask_flag, int32_t* unmasked_pos, int32_t* still_masked_pos,
                   int32_t* counts, int32_t* lane_stats, uint8_t* delim_flag,
                   void* stream);

@@ -23,7 +23,7 @@ STATUS = {0: "AL_OK", -1: "AL_ERR_NULL", -2: "AL_ERR_SHAPE", -3: "AL_ERR_TREE",
           -7: "AL_ERR_HIP"}
 ROLE_GEN, ROLE_REF = 0, 1
 MODE_THRESHOLD, MODE_TOPK = 0, 1
-LANE_STATS = 5
+LANE_STATS = 6
 MAX_SELECT_POSITIONS = 8192
 
 _vp = ctypes.c_void_p
@@ -40,7 +40,7 @@ _SIGNATURES = {
     "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
                                _sz, _vp]),
     "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
-                           _vp, _vp, _i, _i, _f, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+                           _vp, _vp, _i, _i, _f, _i, _f, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
 }
 
 _lib = None
@@ -209,12 +209,12 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
 
 def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=None,
                   t_lane=None, mode=MODE_THRESHOLD, tau=0.9, fallback_k=0, k_lane=None,
-                  delim_ids=(0, 1), eos_id=2, rho_min=0.5, t_min=2, with_delim_flag=True,
-                  out=None):
-    """Per-lane transfer + write-back (tokens / is_masked updated in place),
-    ordered compaction and lane statistics.  Returns a dict of device
-    tensors: unmask_flag, unmasked_pos, still_masked_pos, counts,
-    lane_stats, delim_flag."""
+                  delim_ids=(0, 1), eos_id=2, rho_min=0.5, t_min=2, tau_future=None,
+                  with_delim_flag=True, out=None):
+    """Per-lane transfer, lookahead drafts (tau_future None = off) and
+    write-back (tokens / is_masked updated in place), ordered compaction and
+    lane statistics.  Returns a dict of device tensors: unmask_flag,
+    unmasked_pos, still_masked_pos, counts, lane_stats, delim_flag."""
     lib = library()
     N = int(row_pos.shape[0])
     dev = tokens.device
@@ -236,7 +236,8 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
         _ptr(tokens), _ptr(is_masked), L, B, _np_ptr(role_h), _np_ptr(b_len_h), _np_ptr(t_lane_h),
         int(mode), float(tau), int(fallback_k), _np_ptr(k_lane_h),
         _np_ptr(delim_h) if len(delim_h) else None, len(delim_h), int(eos_id), float(rho_min),
-        int(t_min), _ptr(out["unmask_flag"]), _ptr(out["unmasked_pos"]),
+        int(t_min), float("inf") if tau_future is None else float(tau_future),
+        _ptr(out["unmask_flag"]), _ptr(out["unmasked_pos"]),
         _ptr(out["still_masked_pos"]), _ptr(out["counts"]), _ptr(out["lane_stats"]),
         _ptr(out["delim_flag"]), _stream())
     _check(st, "select_unmask")

@@ -123,14 +123,15 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
                   int32_t* tokens, uint8_t* is_masked, int L, int B, const uint8_t* role,
                   const int32_t* b_len, const int32_t* t_lane, int mode, float tau, int fallback_k,
                   const int32_t* k_lane, const int32_t* delim_ids, int n_delim, int eos_id,
-                  float rho_min, int t_min, uint8_t* unmask_flag, int32_t* unmasked_pos,
+                  float rho_min, int t_min, float tau_future, uint8_t* unmask_flag,
+                  int32_t* unmasked_pos,
                   int32_t* still_masked_pos, int32_t* counts, int32_t* lane_stats,
                   uint8_t* delim_flag, void* stream) {
   if (L < 1 || L > AL_MAX_LANES || B < 1 || (long long)L * B > al::kSelMaxPositions)
     return AL_ERR_SHAPE;
   if (N < 0 || N > L * B) return AL_ERR_SHAPE;
   if (mode != AL_MODE_THRESHOLD && mode != AL_MODE_TOPK) return AL_ERR_SHAPE;
-  if (isnan(tau) || isnan(rho_min) || fallback_k < 0 || n_delim < 0 || n_delim > AL_MAX_DELIMS)
+  if (isnan(tau) || isnan(rho_min) || isnan(tau_future) || fallback_k < 0 || n_delim < 0 || n_delim > AL_MAX_DELIMS)
     return AL_ERR_SHAPE;
   if (!tokens || !is_masked || !role || !counts || !lane_stats) return AL_ERR_NULL;
   if (n_delim > 0 && !delim_ids) return AL_ERR_NULL;
@@ -147,6 +148,7 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
   h.N = N;
   h.mode = mode;
   h.tau = tau;
+  h.tau_future = tau_future;
   h.fallback_k = fallback_k;
   h.eos_id = eos_id;
   h.rho_min = rho_min;

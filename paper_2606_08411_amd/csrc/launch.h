@@ -33,7 +33,7 @@ constexpr int kSelMaxLanes = 64;
 constexpr int kSelMaxDelims = 16;
 struct SelHost {
   int L, B, N, mode, fallback_k, eos_id, t_min, n_delim;
-  float tau, rho_min;
+  float tau, rho_min, tau_future;
   int32_t delim[kSelMaxDelims];
   uint8_t role[kSelMaxLanes];
   int32_t b_len[kSelMaxLanes];

@@ -1,11 +1,15 @@
-// Per-lane transfer selection, write-back, ordered compaction and lane
-// boundary statistics for gfx950 -- one workgroup of 16 wavefronts.
+// Per-lane transfer selection, lookahead drafts, write-back, ordered
+// compaction and lane boundary statistics for gfx950 -- one workgroup of 16
+// wavefronts.
 //
 // Paper Section 3.2: each lane applies the block-wise sampler's confidence
 // rule inside its valid update region [0, b_len); transferred positions take
-// their argmax token and are written back; the lane's split point
-// (eq. split_point), fill ratio and step condition (eq. fork_condition) and
-// valid prefix length ("Advancement control") are read on the updated state.
+// their argmax token and are written back; masked positions of a generate
+// lane's lookahead window [b_len, B) whose confidence reaches tau_future
+// and whose prediction is not EOS are written back as drafts ("Advancement
+// control", eq. lane_input); the lane's split point (eq. split_point), fill
+// ratio and step condition (eq. fork_condition) and valid prefix length
+// ("Advancement control") are read on the updated state.
 //
 // The whole step touches a few KB, so it is latency-bound: one workgroup
 // reads every input once into LDS (one memory latency instead of one per
@@ -36,6 +40,11 @@ struct SelParams {
   uint8_t* delim_flag;
 };
 
+// Per-row selection bits in LDS.
+constexpr uint8_t SEL_TRANSFER = 1;   // chosen by the transfer rule
+constexpr uint8_t SEL_CANDIDATE = 2;  // masked, inside [0, b_len)
+constexpr uint8_t SEL_DRAFT = 4;      // lookahead draft
+
 __device__ __forceinline__ int wave_sum(int v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
@@ -55,12 +64,12 @@ __device__ __forceinline__ int wave_min(int v) {
 __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p) {
   __shared__ int s_tok[kSelMaxPositions];
   __shared__ uint8_t s_msk[kSelMaxPositions];
-  __shared__ uint8_t s_sel[kSelMaxPositions];  // bit0 selected, bit1 candidate
+  __shared__ uint8_t s_sel[kSelMaxPositions];  // SEL_* bits
   __shared__ int s_pos[kSelMaxPositions];      // row_pos
   __shared__ float s_conf[kSelMaxPositions];
   __shared__ int s_arg[kSelMaxPositions];
   __shared__ int s_lo[kSelMaxLanes], s_hi[kSelMaxLanes], s_cnt[kSelMaxLanes], s_nsel[kSelMaxLanes];
-  __shared__ int s_blen[kSelMaxLanes], s_k[kSelMaxLanes];
+  __shared__ int s_blen[kSelMaxLanes], s_k[kSelMaxLanes], s_role[kSelMaxLanes], s_ndraft[kSelMaxLanes];
   __shared__ int s_wu[SEL_WAVES], s_ws[SEL_WAVES];
 
   const SelHost& h = p.h;
@@ -85,6 +94,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     s_nsel[tid] = 0;
     s_blen[tid] = tid < L ? h.b_len[tid] : 0;
     s_k[tid] = tid < L ? h.k_lane[tid] : 0;
+    s_role[tid] = tid < L ? h.role[tid] : 1;
+    s_ndraft[tid] = 0;
   }
   __syncthreads();
 
@@ -97,11 +108,15 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     if (n == 0 || s_pos[n - 1] / B != ln) s_lo[ln] = n;
     if (n == N - 1 || s_pos[n + 1] / B != ln) s_hi[ln] = n + 1;
     const bool cand = i < s_blen[ln] && s_msk[pos];
-    uint8_t f = cand ? 2 : 0;
+    uint8_t f = cand ? SEL_CANDIDATE : 0;
     if (h.mode == 0 && cand && s_conf[n] >= h.tau) {
-      f |= 1;
+      f |= SEL_TRANSFER;
       atomicAdd(&s_cnt[ln], 1);
     }
+    // Lookahead window of a generate lane (tau_future > 1 never passes).
+    if (s_role[ln] == 0 && i >= s_blen[ln] && s_msk[pos] && s_conf[n] >= h.tau_future &&
+        s_arg[n] != h.eos_id)
+      f |= SEL_DRAFT;
     s_sel[n] = f;
   }
   __syncthreads();
@@ -109,7 +124,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   // Top-k (TOPK mode) or fallback (THRESHOLD mode, lanes with no pass):
   // a candidate is chosen when fewer than k candidates of its lane beat it.
   for (int n = tid; n < N; n += SEL_THREADS) {
-    if (!(s_sel[n] & 2)) continue;
+    if (!(s_sel[n] & SEL_CANDIDATE)) continue;
     const int pos = s_pos[n];
     const int ln = pos / B;
     const int k = (h.mode == 1) ? s_k[ln] : (s_cnt[ln] == 0 ? h.fallback_k : 0);
@@ -117,26 +132,28 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     const float c = s_conf[n];
     int rank = 0;
     for (int m = s_lo[ln]; m < s_hi[ln]; ++m) {
-      if (!(s_sel[m] & 2)) continue;
+      if (!(s_sel[m] & SEL_CANDIDATE)) continue;
       const float cm = s_conf[m];
       rank += (cm > c) || (cm == c && s_pos[m] < pos);
     }
-    if (rank < k) s_sel[n] |= 1;
+    if (rank < k) s_sel[n] |= SEL_TRANSFER;
   }
   __syncthreads();
 
-  // Write-back.
+  // Write-back of transfers (flag 1) and drafts (flag 2).
   for (int n = tid; n < N; n += SEL_THREADS) {
-    const int sel = s_sel[n] & 1;
-    p.unmask_flag[n] = (uint8_t)sel;
-    if (sel) {
+    const uint8_t f = s_sel[n];
+    const bool tr = f & SEL_TRANSFER;
+    const bool dr = f & SEL_DRAFT;
+    p.unmask_flag[n] = (uint8_t)(tr ? 1 : (dr ? 2 : 0));
+    if (tr || dr) {
       const int pos = s_pos[n];
       const int tok = s_arg[n];
       p.tokens[pos] = tok;
       p.is_masked[pos] = 0;
       s_tok[pos] = tok;
       s_msk[pos] = 0;
-      atomicAdd(&s_nsel[pos / B], 1);
+      atomicAdd(tr ? &s_nsel[pos / B] : &s_ndraft[pos / B], 1);
     }
   }
   __syncthreads();
@@ -145,7 +162,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   int base_u = 0, base_s = 0;
   for (int b0 = 0; b0 < N; b0 += SEL_THREADS) {
     const int n = b0 + tid;
-    const bool fu = n < N && (s_sel[n] & 1);
+    const bool fu = n < N && (s_sel[n] & (SEL_TRANSFER | SEL_DRAFT));
     const bool fs = n < N && !fu && s_msk[s_pos[n]];
     const unsigned long long bu = __ballot(fu);
     const unsigned long long bs = __ballot(fs);
@@ -201,12 +218,13 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
       const int split = last + 1;
       const bool fork = h.role[ln] == 0 && split > 0 &&
                         (float)filled >= h.rho_min * (float)n && h.t_lane[ln] >= h.t_min;
-      int32_t* st = p.lane_stats + ln * 5;
+      int32_t* st = p.lane_stats + ln * 6;
       st[0] = split;
       st[1] = filled;
       st[2] = stop;
       st[3] = fork ? 1 : 0;
       st[4] = s_nsel[ln];
+      st[5] = s_ndraft[ln];
     }
   }
 }

@@ -17,17 +17,18 @@ pytestmark = pytest.mark.gpu
 
 
 def _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, mode, tau, fb,
-              k_lane, delim=(0, 1), eos=2, rho=0.5, tmin=2):
+              k_lane, delim=(0, 1), eos=2, rho=0.5, tmin=2, tau_future=None):
     import paper_2606_08411_amd as al
     tok_d = dev(tokens)
     msk_d = dev(is_masked)
     out = al.select_unmask(dev(conf), dev(arg), dev(row_pos), tok_d, msk_d, L, B, role, b_len,
-                           t_lane, mode, tau, fb, k_lane, delim, eos, rho, tmin)
+                           t_lane, mode, tau, fb, k_lane, delim, eos, rho, tmin, tau_future)
     torch.cuda.synchronize()
     ref = oracle.select.select_unmask(conf, arg, row_pos, tokens, is_masked, B, role,
                                       b_len if b_len is not None else np.full(L, B),
                                       t_lane if t_lane is not None else np.zeros(L, np.int32),
-                                      mode, tau, fb, k_lane, delim, eos, rho, tmin)
+                                      mode, tau, fb, k_lane, delim, eos, rho, tmin,
+                                      tau_future=tau_future)
     N = len(row_pos)
     cu, cs = out["counts"].cpu().numpy()
     assert [cu, cs] == list(ref["counts"])
@@ -57,6 +58,7 @@ def test_select_workloads(name, ties, step_cache):
 
 def test_select_random_states():
     rng = np.random.default_rng(17)
+    drafts = 0
     for trial in range(40):
         L = int(rng.integers(1, 65))
         B = int(rng.choice([1, 3, 8, 16, 32, 64, 100]))
@@ -76,8 +78,28 @@ def test_select_random_states():
         tau = float(rng.choice([0.0, 0.5, 0.75, 1.0, 2.0]))
         rho = float(rng.choice([0.0, 0.25, 0.5, 0.6, 1.0]))
         mode = trial % 3 == 0
-        _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, int(mode), tau,
-                  int(rng.integers(0, 3)), k_lane, (0, 1, 5), 2, rho, 2)
+        tau_future = [None, 0.0, 0.5, 0.75, 1.0, 1.5][trial % 6]
+        ref = _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, int(mode),
+                        tau, int(rng.integers(0, 3)), k_lane, (0, 1, 5), 2, rho, 2, tau_future)
+        drafts += int((ref["unmask_flag"] == 2).sum())
+    assert drafts > 0   # the lookahead path was exercised
+
+
+@pytest.mark.parametrize("name", ["tiny", "llada", "long", "wide"])
+def test_select_lookahead_workloads(name, step_cache):
+    """Generate lanes with a lookahead window: b_len drawn below B, so the
+    rows of [b_len, B) are draft candidates (Section 3.2, "Advancement
+    control")."""
+    s = step_cache(name, 0, with_weight=False)
+    rng = np.random.default_rng(5)
+    b_len = rng.integers(s.B // 4, s.B + 1, s.L).astype(np.int32)
+    conf, arg = synth.random_confidences(2, s.N, s.V, tie_levels=8)
+    arg[::5] = 2   # EOS predictions are never drafted
+    ref = None
+    for tf in (0.9, 0.5, 0.0):
+        ref = _run_both(conf, arg, s.row_pos, s.tokens, s.is_masked, s.L, s.B, s.role, b_len,
+                        s.t_lane, 0, s.tau, 1, None, tau_future=tf)
+    assert (ref["unmask_flag"] == 2).any()
 
 
 def test_select_empty_and_full():
