@@ -62,8 +62,16 @@ __device__ __forceinline__ int vt_pos4(int k4) {  // k4 = kk / 4, returns pos of
   return 16 * (k4 >> 2) + 8 * (q & 1) + 4 * (q >> 1);
 }
 
+// Two wavefronts per SIMD (<= 256 registers each, no spills at D = 128):
+// with two workgroups per CU, one workgroup's tile staging (loads, the
+// transposed V store, barriers) overlaps the other's MFMAs.  At one
+// wavefront per SIMD (312 registers) the phases serialize: 530 us vs
+// 270 us on the Wide lane pass (MI355X).
+constexpr int AT_OCC = 2;
+
 template <int D>
-__global__ __launch_bounds__(AT_THREADS) void lane_attn_kernel(AttnParams p) {
+__global__ __launch_bounds__(AT_THREADS) __attribute__((amdgpu_waves_per_eu(AT_OCC, AT_OCC)))
+void lane_attn_kernel(AttnParams p) {
   constexpr int KS = D / 16;       // MFMA k-steps of S^T = K Q^T
   constexpr int DT = D / 32;       // 32-row tiles of O^T
   constexpr int KSTR = D + 8;      // bf16 per K row in LDS (+16 B: spreads banks)
@@ -381,13 +389,14 @@ __global__ __launch_bounds__(256) void prefix_scatter_kernel(const int32_t* idx,
 
 // ------------------------------------------------------------------ host
 static int choose_split(int base_wgs, int total_key_tiles) {
-  // Short grids leave most of the 256 CUs idle: split the key tiles (each
-  // split keeps at least one tile) until about 128 workgroups exist.  More
-  // splits shorten each workgroup's key loop but add partials to merge; on
-  // the LLaDA step shape (40 base workgroups) 4 splits take 22.9 us with
-  // the merge, 8 take 24.7 us and 2 take 29.9 us (MI355X).
+  // Short grids leave CUs idle: split the key tiles until about 512
+  // workgroups exist (two per CU at two wavefronts per SIMD), keeping at
+  // least 3 key tiles per split, since each split adds partials to merge.
+  // Measured with the merge (MI355X, best in [1, 16]): LLaDA step shape
+  // 4 splits, 21.4 us; Dream 8, 29.1 us; Long 4, 62.8 us (128 us
+  // unsplit); Wide 1, 277 us.
   int s = 1;
-  while (s < 8 && base_wgs * s < 128 && 2 * s <= total_key_tiles) s *= 2;
+  while (s < 16 && base_wgs * s < 512 && total_key_tiles >= 3 * (2 * s)) s *= 2;
   return s;
 }
 
