@@ -164,7 +164,8 @@ int lane_attn_forward(const al_bf16* q, const al_bf16* k_lane, const al_bf16* v_
  * workspace dev, >= lmhead_confidence_workspace_size(N, d, V) bytes of
  *          scratch (per-vocab-tile partial maxima, sums and indices);
  *          contents need not be initialised.  Calls that share a workspace
- *          must not run concurrently.
+ *          must not run concurrently.  The size depends on the compute-unit
+ *          count of the current device: query it with that device current.
  * ------------------------------------------------------------------------ */
 size_t lmhead_confidence_workspace_size(int N, int d, int V);
 

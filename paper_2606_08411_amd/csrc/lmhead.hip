@@ -8,17 +8,15 @@
 // suppress EOS).
 //
 // The step streams the whole weight W ([V][d] bf16, ~1 GB at V=126464,
-// d=4096) once for a few hundred hidden rows, so lmhead_partial_kernel is
-// shaped for HBM streaming rather than for MFMA reuse (measured on MI355X):
-// * each wavefront owns 16 vocabulary rows (the A operand of the 16x16x32
-//   bf16 MFMA); per chunk it loads 256 contiguous bytes of each row
-//   (4 instructions x 4 lanes x 16 B, issued back to back) straight into
-//   registers, two chunks ahead of the MFMAs -- each W element is used by
-//   one wavefront only;
-// * the chunk of the scored hidden rows (B operand, <= 128 rows) is staged
-//   once per workgroup in LDS and shared by its wavefronts; the LDS buffer
-//   is small enough for several workgroups per CU, which keeps enough W
-//   loads in flight;
+// d=4096) for a few tens to a few hundred hidden rows, so
+// lmhead_partial_kernel is shaped for HBM streaming first and MFMA reuse
+// second (measured on MI355X):
+// * each wavefront owns 32 vocabulary rows (the A operand of the 32x32x16
+//   bf16 MFMA) and loads them straight into registers, two chunks ahead;
+//   each W element is used by one wavefront only;
+// * the chunk of the scored hidden rows (B operand, <= 224 rows per column
+//   tile; more rows take several tiles, each streaming W again) is staged
+//   once per workgroup in LDS and shared by its 8 wavefronts;
 // * workgroups are dealt to the 8 XCDs in contiguous runs of vocab tiles;
 // * the epilogue writes one partial (m, s, argmax) per column and vocab
 //   tile; lmhead_merge_kernel combines them in a fixed order, so results
@@ -32,7 +30,7 @@
 
 namespace al {
 
-constexpr int LM_MAX_FRAG = 8;   // <= 128 scored rows per column tile
+constexpr int LM_MAX_NF = 7;     // <= 224 scored rows per column tile
 constexpr float LM_LOG2E = 1.4426950408889634f;
 
 struct LmPartial {
@@ -49,6 +47,7 @@ struct LmParams {
   const uint8_t* sup;
   LmPartial* part;  // [n_nt][nt_cols][n_vt]: a row's partials are contiguous
   int N, d, V, eos_id;
+  // Vocab tile vt covers rows [vt*V/n_vt, (vt+1)*V/n_vt) (<= 32*WAVES rows).
   int n_vt, n_nt, nt_cols, tiles_total, tiles_per_xcd;
 };
 
@@ -69,30 +68,37 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
   m = M;
 }
 
-// WAVES wavefronts x 16 vocab rows per workgroup.  W is streamed in chunks
-// of KC hidden elements (each lane loads KC/4 contiguous elements of its row
-// per chunk, PF chunks ahead of the MFMAs, so the MFMA work overlaps the
-// stream).  The hidden chunk is staged once per workgroup in LDS.
-// OCC: wavefronts per SIMD the register allocation must allow.
-template <int NFRAG, bool RAGGED, int WAVES, int KC, int PF, int OCC>
-__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+// WAVES wavefronts x 32 vocab rows per workgroup (VT = 32*WAVES), NF
+// 32-column fragments (NT = 32*NF scored rows) per tile, 32x32x16 bf16 MFMA.
+// * W streams straight into registers, KC elements per chunk, PF chunks
+//   ahead (lane half h of row r takes K elements kc + 16s + 8h .. +8; over
+//   a chunk each row is read as one 2*KC-byte run).  Each W element is used
+//   by one wavefront only.
+// * The hidden chunk (NT x KC) is double-buffered in LDS, one barrier per
+//   chunk, and shared by the workgroup's wavefronts.  Its loads go into a
+//   two-deep register ring issued two chunks ahead and before the W
+//   prefetch, so the wait for them (the load counter is in-order) never
+//   waits for W loads that are still needed later.
+// * 32-row A tiles halve the B-operand LDS reads per FLOP of 16x16x32
+//   steps, and 256 vocab rows per workgroup keep the hidden-chunk traffic
+//   at NT/256 of the W traffic.
+// * Two wavefronts per SIMD: the accumulators take 16*NF registers.
+template <int NF, bool RAGGED, int WAVES, int KC, int PF>
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
   constexpr int THREADS = WAVES * 64;
-  constexpr int VT = 16 * WAVES;                 // vocab rows per workgroup
-  constexpr int STEPS = KC / 32;                 // MFMA k-steps per chunk
-  constexpr int KCH = KC;                        // hidden elements staged at once
-  constexpr int NT = 16 * NFRAG;                 // scored rows (columns) per tile
-  constexpr int KSEG = KCH / 8;                  // 16-byte segments per staged row
-  // bf16 per staged row: +32 B of padding makes the B-operand reads below
-  // conflict-free (measured on gfx950; +16 B costs 2x in bank conflicts).
-  constexpr int STRIDE = KCH + 16;
+  constexpr int VT = 32 * WAVES;                 // vocab rows per workgroup
+  constexpr int STEPS = KC / 16;                 // MFMA k-steps per chunk
+  constexpr int NT = 32 * NF;                    // scored rows (columns) per tile
+  constexpr int KSEG = KC / 8;                   // 16-byte segments per staged row
+  // +16 B per staged row: the 32 rows read by one half-wavefront start
+  // 4 banks apart, so the B-operand reads are conflict-free.
+  constexpr int STRIDE = KC + 8;
   constexpr int SEGS = NT * KSEG;
   constexpr int HREG = (SEGS + THREADS - 1) / THREADS;
-  // Rows past NT are written (by the last staging pass) but never read:
-  // every thread stores, so the staging code has no divergent branch.
   constexpr int ROWS_STAGED = HREG * THREADS / KSEG;
-  __shared__ __attribute__((aligned(16))) uint16_t hs[ROWS_STAGED * STRIDE];
-  // After the K loop the staging buffer holds the per-wavefront (m, s, idx).
+  constexpr int BUF = ROWS_STAGED * STRIDE;
+  __shared__ __attribute__((aligned(16))) uint16_t hs[2 * BUF];
   static_assert(sizeof(hs) >= 3 * sizeof(float) * WAVES * NT, "reduction scratch");
   float (*red_m)[NT] = reinterpret_cast<float (*)[NT]>(&hs[0]);
   float (*red_s)[NT] = red_m + WAVES;
@@ -107,21 +113,19 @@ void lmhead_partial_kernel(LmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
-  const int r16 = lane & 15;
-  const int g4 = lane >> 4;
+  const int r32 = lane & 31;
+  const int h = lane >> 5;
   const int d = p.d;
-  const int v0 = vt * VT + w * 16;
+  const int vb = (int)((long long)vt * p.V / p.n_vt);
+  const int ve = (int)((long long)(vt + 1) * p.V / p.n_vt);
+  const int v0 = vb + w * 32;
   const int n0 = nt * p.nt_cols;
   const int ncols = min(NT, p.N - n0);
 
-  // Loads are unconditional and in bounds (clamped addresses); values are
-  // not post-processed after loading.  A W segment past d meets hidden
-  // values zeroed at the LDS store; rows past V are dropped in the epilogue.
-  const uint16_t* wrow = p.W + (size_t)min(v0 + r16, p.V - 1) * d;
-  const uint16_t* wlane = wrow + g4 * 8;
-  // Hidden staging: thread tid moves segments tid + THREADS*i of the
-  // NT x KSEG staged block (row-major); 32-bit row offsets (n_rows * d <
-  // 2^31 is checked by the caller).
+  // Rows past the tile read its last row (cache hits; dropped in the
+  // epilogue).
+  const uint16_t* wrow = p.W + (size_t)min(v0 + r32, ve - 1) * d;
+  const uint16_t* wlane = wrow + h * 8;
   unsigned hoff[HREG];
   int hcol[HREG];
   int hdst[HREG];
@@ -139,116 +143,98 @@ void lmhead_partial_kernel(LmParams p) {
     hvalid |= (ok ? 1u : 0u) << i;
   }
 
-  f32x4 acc[NFRAG];
+  f32x16 acc[NF];
 #pragma unroll
-  for (int f = 0; f < NFRAG; ++f)
+  for (int f = 0; f < NF; ++f)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[f][r] = 0.f;
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.f;
 
-  bf16x8 wr[PF + 1][STEPS], hr[HREG];
-  // Step s of a chunk covers K elements kc + s*32 .. +32; lane group g4
-  // takes kc + s*32 + g4*8 .. +8 on both operands, so each W load
-  // instruction reads 64 contiguous bytes of every row of the wavefront.
+  constexpr int RING = PF + 1;   // W register slots (chunks)
+  bf16x8 wr[RING][STEPS], hr[2][HREG];
+  auto load_w1 = [&](int kc, int s) {
+    if (RAGGED) {
+      const int k = kc + s * 16 + h * 8;
+      return load_bf16x8(wrow + (k < d ? k : 0));
+    }
+    return load_bf16x8(wlane + kc + s * 16);
+  };
   auto load_w = [&](bf16x8* wv, int kc) {
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      if (RAGGED) {
-        const int k = kc + s * 32 + g4 * 8;
-        wv[s] = load_bf16x8(wrow + (k < d ? k : 0));
-      } else {
-        wv[s] = load_bf16x8(wlane + kc + s * 32);
-      }
-    }
+    for (int s = 0; s < STEPS; ++s) wv[s] = load_w1(kc, s);
   };
-  // Hidden segment i of the block starting at kh covers element
-  // hcol[i] + kh of its row; past d it reads the row start instead and is
-  // zeroed at the LDS store.
-  auto load_h = [&](int kh) {
+  auto load_h = [&](bf16x8* hv, int kh) {
 #pragma unroll
     for (int i = 0; i < HREG; ++i) {
       if (RAGGED)
-        hr[i] = load_bf16x8(p.hidden + (hcol[i] + kh < d ? hoff[i] + kh : hoff[i] - hcol[i]));
+        hv[i] = load_bf16x8(p.hidden + (hcol[i] + kh < d ? hoff[i] + kh : hoff[i] - hcol[i]));
       else
-        hr[i] = load_bf16x8(p.hidden + (hoff[i] + kh));
+        hv[i] = load_bf16x8(p.hidden + (hoff[i] + kh));
     }
   };
-  // Zeroing past d and for unused columns happens at the LDS store, where
-  // the data is awaited anyway (a select right after a load would stall).
-  auto store_h = [&](int kh) {
+  auto store_h = [&](const bf16x8* hv, uint16_t* buf, int kh) {
 #pragma unroll
     for (int i = 0; i < HREG; ++i) {
       const bool kin = !RAGGED || hcol[i] + kh < d;
-      *reinterpret_cast<bf16x8*>(&hs[hdst[i]]) = (kin && ((hvalid >> i) & 1u)) ? hr[i] : zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&buf[hdst[i]]) = (kin && ((hvalid >> i) & 1u)) ? hv[i] : zero_bf16x8();
     }
   };
-  // MFMA step s covers, for lane group g4, the K elements
-  // kc + s*32 + g4*8 + e (e = 0..7) on both operands.
-  auto mma = [&](const bf16x8* wv) {
+  auto mma = [&](const bf16x8* wv, const uint16_t* buf) {
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
 #pragma unroll
-      for (int f = 0; f < NFRAG; ++f) {
-        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(
-            &hs[(f * 16 + r16) * STRIDE + s * 32 + g4 * 8]);
-        acc[f] = mfma16x16x32(wv[s], bv, acc[f]);
+      for (int f = 0; f < NF; ++f) {
+        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(&buf[(f * 32 + r32) * STRIDE + s * 16 + h * 8]);
+        acc[f] = mfma32x32x16(wv[s], bv, acc[f]);
       }
     }
   };
 
-  // Chunk c uses register buffer c % (PF+1); W(c+PF) is prefetched while
-  // chunk c is multiplied.  The next hidden chunk's loads are issued before
-  // that prefetch (the load counter is in-order and the LDS store waits for
-  // them).  The steady-state loop has every prefetch in range and no
-  // branches; the last chunks are peeled.
+  // Chunk c: W in register slot c % RING, hidden chunk in LDS buffer
+  // c % 2, hidden registers hr[c % 2] receive chunk c+2.
   const int nch = (d + KC - 1) / KC;
-  load_h(0);
+  load_h(hr[0], 0);
+  if (nch > 1) load_h(hr[1], KC);
 #pragma unroll
   for (int j = 0; j < PF; ++j)
     if (j < nch) load_w(wr[j], j * KC);
-  store_h(0);
+  store_h(hr[0], hs, 0);
   __syncthreads();
-  auto chunk_full = [&](int c, const bf16x8* cur, bf16x8* pre) {
-    load_h((c + 1) * KC);
-    load_w(pre, (c + PF) * KC);
+  auto chunk = [&](int c, const bf16x8* cur, bf16x8* pre, bf16x8* h_next, bf16x8* h_free, bool full) {
+    // h_next holds chunk c+1 (loaded two chunks ago); h_free receives c+2.
+    if (full || c + 2 < nch) load_h(h_free, (c + 2) * KC);
+    if (full || c + PF < nch) load_w(pre, (c + PF) * KC);
     __builtin_amdgcn_sched_barrier(0);
-    mma(cur);
-    __syncthreads();  // every wavefront is done with this hidden chunk
-    store_h((c + 1) * KC);
+    mma(cur, hs + (c & 1) * BUF);
+    if (full || c + 1 < nch) store_h(h_next, hs + ((c + 1) & 1) * BUF, (c + 1) * KC);
     __syncthreads();
   };
-  auto chunk_tail = [&](int c, const bf16x8* cur, bf16x8* pre) {
-    const bool has_next = c + 1 < nch;
-    if (has_next) load_h((c + 1) * KC);
-    if (c + PF < nch) load_w(pre, (c + PF) * KC);
-    mma(cur);
-    if (has_next) {
-      __syncthreads();
-      store_h((c + 1) * KC);
-      __syncthreads();
-    }
-  };
+  // Steady state: unrolled over lcm(RING, 2) chunks so every register
+  // index is static; all loads in range (c + max(PF, 2) < nch).
+  constexpr int U = RING % 2 == 0 ? RING : 2 * RING;
+  constexpr int AHEAD = PF > 2 ? PF : 2;
   int c = 0;
-  for (; c + 2 * PF < nch; c += PF + 1) {
+  for (; c + U - 1 + AHEAD < nch; c += U) {
 #pragma unroll
-    for (int j = 0; j <= PF; ++j) chunk_full(c + j, wr[j], wr[(j + PF) % (PF + 1)]);
+    for (int j = 0; j < U; ++j)
+      chunk(c + j, wr[j % RING], wr[(j + PF) % RING], hr[(j + 1) & 1], hr[j & 1], true);
   }
 #pragma unroll
-  for (int j = 0; j < 2 * PF + 1; ++j)
-    if (c + j < nch) chunk_tail(c + j, wr[j % (PF + 1)], wr[(j + PF) % (PF + 1)]);
-  __syncthreads();
+  for (int j = 0; j < U - 1 + AHEAD; ++j)
+    if (c + j < nch)
+      chunk(c + j, wr[j % RING], wr[(j + PF) % RING], hr[(j + 1) & 1], hr[j & 1], false);
 
-  // Epilogue: lane (r16, g4) holds vocab rows v0 + 4*g4 + r (r = 0..3) of
-  // column n0 + f*16 + r16.
+  // Epilogue: lane (r32, h) holds vocab rows v0 + 8*(r/4) + 4h + r%4
+  // (r = 0..15) of column n0 + 32f + r32.
 #pragma unroll
-  for (int f = 0; f < NFRAG; ++f) {
-    const int n = n0 + f * 16 + r16;
+  for (int f = 0; f < NF; ++f) {
+    const int n = n0 + f * 32 + r32;
     const bool sup_row = (n < p.N) && p.sup && p.sup[n];
     float m = -INFINITY;
     int idx = 0x7fffffff;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int v = v0 + 4 * g4 + r;
-      const bool ok = v < p.V && !(sup_row && v == p.eos_id);
+    for (int r = 0; r < 16; ++r) {
+      const int v = v0 + 8 * (r >> 2) + 4 * h + (r & 3);
+      const bool ok = v < ve && !(sup_row && v == p.eos_id);
       if (ok && acc[f][r] > m) {
         m = acc[f][r];
         idx = v;
@@ -257,20 +243,18 @@ void lmhead_partial_kernel(LmParams p) {
     float s = 0.f;
     if (m != -INFINITY) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int v = v0 + 4 * g4 + r;
-        const bool ok = v < p.V && !(sup_row && v == p.eos_id);
+      for (int r = 0; r < 16; ++r) {
+        const int v = v0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const bool ok = v < ve && !(sup_row && v == p.eos_id);
         if (ok) s += exp2_fast((acc[f][r] - m) * LM_LOG2E);
       }
     }
-    merge_state(m, s, idx, __shfl_xor(m, 16, kWave), __shfl_xor(s, 16, kWave),
-                __shfl_xor(idx, 16, kWave));
     merge_state(m, s, idx, __shfl_xor(m, 32, kWave), __shfl_xor(s, 32, kWave),
                 __shfl_xor(idx, 32, kWave));
-    if (g4 == 0) {
-      red_m[w][f * 16 + r16] = m;
-      red_s[w][f * 16 + r16] = s;
-      red_i[w][f * 16 + r16] = idx;
+    if (h == 0) {
+      red_m[w][f * 32 + r32] = m;
+      red_s[w][f * 32 + r32] = s;
+      red_i[w][f * 32 + r32] = idx;
     }
   }
   __syncthreads();
@@ -335,26 +319,46 @@ __global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
 
 // ------------------------------------------------------------------ host
 constexpr int LM_WAVES = 8;
-constexpr int LM_KC = 128;
-// Prefetch depth: two W chunks in flight where registers allow (up to 96
-// scored columns), one beyond that (no spills at 128 columns).
-constexpr int lm_pf(int nfrag) { return nfrag <= 6 ? 2 : 1; }
-constexpr int LM_OCC = 4;
-constexpr int LM_VT = 16 * LM_WAVES;
+constexpr int LM_VT = 32 * LM_WAVES;
+// Chunk size per fragment count (no register spills at two wavefronts per
+// SIMD): 256-byte W runs up to 128 columns, 128-byte runs above.
+constexpr int lm_kc(int nf) { return nf <= 4 ? 128 : 64; }
+constexpr int LM_PF = 2;
 
-// Column tiling: n_nt tiles of nfrag 16-column fragments (<= 128 columns).
+// Column tiling: n_nt tiles of nf 32-column fragments (<= 224 columns).
 struct LmLayout {
-  int nfrag, nt_cols, n_nt, n_vt;
+  int nf, nt_cols, n_nt, n_vt;
   size_t total;
 };
 
+// Compute units of the current device (cached per device).
+static int lm_cu_count() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 static LmLayout lm_layout(int N, int V) {
   LmLayout L{};
-  const int frags = N > 0 ? (N + 15) / 16 : 1;
-  L.n_nt = N > 0 ? (frags + LM_MAX_FRAG - 1) / LM_MAX_FRAG : 0;
-  L.nfrag = N > 0 ? (frags + L.n_nt - 1) / L.n_nt : 1;
-  L.nt_cols = 16 * L.nfrag;
-  L.n_vt = (V + LM_VT - 1) / LM_VT;
+  const int frags = N > 0 ? (N + 31) / 32 : 1;
+  L.n_nt = N > 0 ? (frags + LM_MAX_NF - 1) / LM_MAX_NF : 0;
+  L.nf = N > 0 ? (frags + L.n_nt - 1) / L.n_nt : 1;
+  L.nt_cols = 32 * L.nf;
+  // One workgroup per CU runs at a time.  When the vocabulary needs more
+  // than one round of LM_VT-row tiles, the tile count is rounded up to a
+  // multiple of the CU count and the rows are spread evenly, so the last
+  // round is not partly empty (V = 152064: 594 full tiles would take 3
+  // rounds at 77% use; 768 tiles of 198 rows take 3 even rounds).
+  const int base = (V + LM_VT - 1) / LM_VT;
+  const int units = lm_cu_count();
+  L.n_vt = base <= units ? base : units * ((base + units - 1) / units);
   L.total = sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
   return L;
 }
@@ -387,26 +391,26 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.tiles_total = L.n_vt * L.n_nt;
   p.tiles_per_xcd = (p.tiles_total + 7) / 8;
   const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
-  const bool ragged = d % LM_KC != 0;
+  // The plain kernel assumes d % KC == 0; other d take the RAGGED variant.
+  const bool ragged = d % lm_kc(L.nf) != 0;
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), LM_OCC>), grid, block, 0,  \
-                         stream, p);                                                          \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, lm_kc(F), LM_PF>), grid,   \
+                         block, 0, stream, p);                                                \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), LM_OCC>), grid, block, 0, \
-                         stream, p);                                                          \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, lm_kc(F), LM_PF>), grid,  \
+                         block, 0, stream, p);                                                \
     break;
-  switch (L.nfrag) {
+  switch (L.nf) {
     AL_LM_CASE(1)
     AL_LM_CASE(2)
     AL_LM_CASE(3)
     AL_LM_CASE(4)
     AL_LM_CASE(5)
     AL_LM_CASE(6)
-    AL_LM_CASE(7)
     default:
-      AL_LM_CASE(8)
+      AL_LM_CASE(7)
   }
 #undef AL_LM_CASE
   hipLaunchKernelGGL(lmhead_merge_kernel, dim3(N), dim3(LM_MERGE_THREADS), 0, stream, p.part, N,
