@@ -18,10 +18,11 @@ Transferred positions take the argmax token and become unmasked.
 Boundary statistics per lane on the updated state (0-indexed positions
 i < b_len; delimiters and EOS as in Section 3.2):
 
-* delim_i   = position i is filled and holds a delimiter id
+* delim_i   = position i is filled, holds a delimiter id and passes
+              ValidBoundary on the prefix [0, i]
 * split     = 1 + the last i with delim_i, or 0 when there is none
-              (eq. split_point with ValidBoundary taken as always true:
-              the 0-indexed start of the continuation lane)
+              (eq. split_point: the 0-indexed start of the continuation
+              lane)
 * n_filled  = number of filled positions (eq. fork_condition's numerator)
 * valid_len = the first i that is masked or holds EOS, or b_len if none
               (the valid prefix length of "Advancement control")
@@ -41,6 +42,15 @@ whose predicted token is not EOS takes that token as a draft (unmask_flag
 draft.  tau_future None (or above 1, since conf <= 1) disables drafting.
 The paper gives no value for tau_future.
 
+ValidBoundary (Section 3.2; the experimental setup of Section 4): the
+paper names numeric-period exclusion for the math tasks and no split inside
+unclosed brackets for code, as predicates of the prefix z_{1:i}.  Read here
+with token-id sets (empty sets: always valid):
+
+* numeric period: invalid when position i-1 is filled with a digit id;
+* bracket balance: invalid when the filled positions of [0, i] hold more
+  open-bracket ids than close-bracket ids.
+
 Decisions that compare floating point values (threshold, ordering, fill
 ratio) are taken in fp32, the precision the device kernel uses.
 """
@@ -55,8 +65,25 @@ STAT_SPLIT, STAT_FILLED, STAT_VALID, STAT_FORK, STAT_NSEL, STAT_NDRAFT = range(6
 N_STATS = 6
 
 
+def valid_boundary(tokens, is_masked, start, i, digit_ids=(), open_ids=(), close_ids=()):
+    """ValidBoundary of the delimiter at lane position i, whose lane block
+    starts at flat position start: a predicate of the prefix [0, i]."""
+    if i > 0 and not is_masked[start + i - 1] and int(tokens[start + i - 1]) in set(digit_ids):
+        return False
+    depth = 0
+    for j in range(i + 1):
+        if is_masked[start + j]:
+            continue
+        t = int(tokens[start + j])
+        if t in set(open_ids):
+            depth += 1
+        elif t in set(close_ids):
+            depth -= 1
+    return depth <= 0
+
+
 def lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane, delim_ids,
-                        eos_id, rho_min, t_min):
+                        eos_id, rho_min, t_min, digit_ids=(), open_ids=(), close_ids=()):
     """Returns (lane_stats [L][6] int32, delim_flag [L*B] uint8); the
     n_sel and n_draft columns are left at zero here."""
     L = len(role)
@@ -74,7 +101,8 @@ def lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane, delim_ids,
             tok = int(tokens[pos])
             if not masked:
                 filled += 1
-                if tok in dset:
+                if tok in dset and valid_boundary(tokens, is_masked, lane * B, i,
+                                                  digit_ids, open_ids, close_ids):
                     dflag[pos] = 1
                     split = i + 1
             if valid == n and (masked or tok == eos_id):
@@ -91,7 +119,8 @@ def lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane, delim_ids,
 
 def select_unmask(conf, argmax, row_pos, tokens, is_masked, B, role, b_len, t_lane,
                   mode, tau, fallback_k=0, k_lane=None, delim_ids=(0, 1), eos_id=2,
-                  rho_min=0.5, t_min=2, tau_future=None):
+                  rho_min=0.5, t_min=2, tau_future=None, digit_ids=(), open_ids=(),
+                  close_ids=()):
     """Per-lane transfer on the rows row_pos (flat positions lane*B + i,
     ascending), lookahead drafts, then the boundary statistics.
 
@@ -137,7 +166,8 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, B, role, b_len, t_la
     still = np.array([row_pos[n] for n in range(N) if not flag[n] and is_masked[row_pos[n]]],
                      dtype=np.int32)
     stats, dflag = lane_boundary_stats(tokens, is_masked, B, role, b_len, t_lane,
-                                       delim_ids, eos_id, rho_min, t_min)
+                                       delim_ids, eos_id, rho_min, t_min,
+                                       digit_ids, open_ids, close_ids)
     for n in range(N):
         if flag[n] == 1:
             stats[row_pos[n] // B, STAT_NSEL] += 1

@@ -658,6 +658,80 @@ def check_lookahead_properties(sel):
         assert prev == want
 
 
+def _id_set(field):
+    if field == "-":
+        return ()
+    out = []
+    for part in field.split(","):
+        if "-" in part:
+            lo, hi = part.split("-")
+            out += list(range(int(lo), int(hi) + 1))
+        else:
+            out.append(int(part))
+    return tuple(out)
+
+
+def check_valid_boundary_golden(sel):
+    """Hand-worked numeric-period and bracket-balance cases
+    (tests/golden/valid_boundary_cases.txt)."""
+    n = 0
+    with open(os.path.join(GOLDEN, "valid_boundary_cases.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            lhs, rhs = line.split("||")
+            toks, b_len, role, t, rho, tmin, dig, opn, cls = [x.strip() for x in lhs.split("|")]
+            split, filled, valid, fork, dpos = [x.strip() for x in rhs.split("|")]
+            tk = toks.split(",")
+            # "M" = masked; "M<id>" = masked position still holding a stale id
+            tokens = np.array([(int(x[1:]) if len(x) > 1 else -1) if x.startswith("M") else int(x)
+                               for x in tk], np.int32)
+            masked = np.array([x.startswith("M") for x in tk], np.uint8)
+            stats, dflag = sel.lane_boundary_stats(
+                tokens, masked, len(tk), np.array([0 if role == "gen" else 1]),
+                np.array([int(b_len)]), np.array([int(t)]), (0, 1), 2, float(rho), int(tmin),
+                _id_set(dig), _id_set(opn), _id_set(cls))
+            want = [int(split), int(filled), int(valid), int(fork)]
+            assert list(stats[0, :4]) == want, (line, stats)
+            assert list(np.flatnonzero(dflag)) == ([int(x) for x in dpos.split(",")] if dpos else []), line
+            n += 1
+    assert n >= 10
+
+
+def check_valid_boundary_properties(sel):
+    """Empty id sets are the plain statistics; a rule can only remove
+    delimiters (split never grows); brackets never inside an open scope."""
+    rng = np.random.default_rng(31)
+    L, B = 5, 24
+    for _ in range(30):
+        tokens = rng.integers(0, 26, L * B).astype(np.int32)
+        masked = (rng.random(L * B) < 0.3).astype(np.uint8)
+        b_len = rng.integers(0, B + 1, L).astype(np.int32)
+        role = rng.integers(0, 2, L).astype(np.uint8)
+        t_lane = rng.integers(0, 4, L).astype(np.int32)
+        base = sel.lane_boundary_stats(tokens, masked, B, role, b_len, t_lane, (0, 1), 2, 0.5, 2)
+        same = sel.lane_boundary_stats(tokens, masked, B, role, b_len, t_lane, (0, 1), 2, 0.5, 2,
+                                       (), (), ())
+        assert np.array_equal(base[0], same[0]) and np.array_equal(base[1], same[1])
+        for sets in [((10, 11, 12), (), ()), ((), (20,), (22,)), ((10, 13), (20, 21), (22, 23))]:
+            st, df = sel.lane_boundary_stats(tokens, masked, B, role, b_len, t_lane, (0, 1), 2,
+                                             0.5, 2, *sets)
+            assert np.all(df <= base[1])
+            assert np.all(st[:, 0] <= base[0][:, 0])
+            assert np.array_equal(st[:, 1:3], base[0][:, 1:3])   # filled, valid_len unchanged
+            for pos in np.flatnonzero(df):
+                lane, i = pos // B, pos % B
+                seg_t = tokens[lane * B:pos + 1]
+                seg_m = masked[lane * B:pos + 1].astype(bool)
+                opens = int(np.isin(seg_t[~seg_m], sets[1]).sum())
+                closes = int(np.isin(seg_t[~seg_m], sets[2]).sum())
+                assert opens <= closes
+                if i > 0 and not masked[pos - 1]:
+                    assert tokens[pos - 1] not in sets[0]
+
+
 SELECT_CHECKS = [check_select_brute_force, check_select_threshold_extremes,
                  check_lane_stats_golden, check_lane_stats_scan,
-                 check_lookahead_golden, check_lookahead_properties]
+                 check_lookahead_golden, check_lookahead_properties,
+                 check_valid_boundary_golden, check_valid_boundary_properties]

@@ -58,8 +58,8 @@ MUTANTS = {
         ("split without +1", "split = i + 1", "split = i"),
         ("valid length off by one", "valid = i\n", "valid = i + 1\n"),
         ("EOS does not end the valid prefix", "(masked or tok == eos_id)", "(masked)"),
-        ("masked delimiters counted", "if not masked:\n                filled += 1\n                if tok in dset:",
-         "if True:\n                filled += not masked\n                if tok in dset:"),
+        ("masked delimiters counted", "if not masked:\n                filled += 1\n                if tok in dset and",
+         "if True:\n                filled += not masked\n                if tok in dset and"),
         ("strict fill ratio", "np.float32(filled) >= np.float32(rho_min)", "np.float32(filled) > np.float32(rho_min)"),
         ("fill ratio in fp64", "np.float32(filled) >= np.float32(rho_min) * np.float32(n)", "filled >= rho_min * n"),
         ("refine lanes fork", "int(role[lane]) == ROLE_GEN and", "True and"),
@@ -76,6 +76,13 @@ MUTANTS = {
         ("drafts counted as transfers", "elif flag[n] == 2:\n            stats[row_pos[n] // B, STAT_NDRAFT] += 1",
          "elif flag[n] == 2:\n            stats[row_pos[n] // B, STAT_NSEL] += 1"),
         ("drafts left out of unmasked_pos", "unmasked_pos = row_pos[flag != 0]", "unmasked_pos = row_pos[flag == 1]"),
+        ("digit test reads the next position", "int(tokens[start + i - 1]) in set(digit_ids)",
+         "start + i + 1 < len(tokens) and int(tokens[start + i + 1]) in set(digit_ids)"),
+        ("digit test ignores the mask", "if i > 0 and not is_masked[start + i - 1] and", "if i > 0 and"),
+        ("strictly negative depth required", "return depth <= 0", "return depth < 0"),
+        ("masked brackets counted", "        if is_masked[start + j]:\n            continue\n", ""),
+        ("close brackets ignored", "depth -= 1", "depth -= 0"),
+        ("ValidBoundary ignored", "if tok in dset and valid_boundary(", "if tok in dset and True or valid_boundary("),
     ],
 }
 
