@@ -67,6 +67,7 @@ typedef uint16_t al_bf16;
 
 #define AL_MAX_LANES 64         /* one ancestor set per lane fits a uint64       */
 #define AL_MAX_DELIMS 16
+#define AL_MAX_BOUNDARY_IDS 32  /* per ValidBoundary id set of select_unmask  */
 #define AL_MAX_SELECT_POSITIONS 8192  /* L*B limit of select_unmask              */
 
 /* lane_stats columns (int32 [L][AL_LANE_STATS]) */
@@ -211,6 +212,14 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
  * mode     AL_MODE_THRESHOLD or AL_MODE_TOPK;  tau fp32 (not NaN)
  * fallback_k >= 0;  k_lane host [L] >= 0 (required in TOPK mode, else unused)
  * delim_ids host [n_delim] token ids, 0 <= n_delim <= AL_MAX_DELIMS
+ * digit_ids, open_ids, close_ids  host [n_digit] / [n_open] / [n_close]
+ *          token ids (each count 0..AL_MAX_BOUNDARY_IDS; NULL when 0) of
+ *          ValidBoundary (Section 3.2, Section 4 setup): a delimiter at
+ *          lane position i counts only if position i-1 is not filled with a
+ *          digit id (numeric-period exclusion) and the filled positions of
+ *          [0, i] hold no more open- than close-bracket ids (no split inside
+ *          unclosed brackets).  Masked positions are neither.  All sets
+ *          empty: every delimiter counts.
  * eos_id   token id ending the valid prefix (-1 = none)
  * rho_min, t_min  fork condition parameters
  * tau_future fp32 (not NaN): lookahead draft threshold, > 1 = off
@@ -222,13 +231,15 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
  * counts   dev [2] int32 out: {#unmasked_pos, #still_masked_pos}
  * lane_stats dev [L][AL_LANE_STATS] int32 out
  * delim_flag dev [L*B] uint8 out or NULL: 1 iff the position is < b_len of
- *          its lane, filled and holds a delimiter id
+ *          its lane, filled, holds a delimiter id and passes ValidBoundary
  * ------------------------------------------------------------------------ */
 int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_pos, int N,
                   int32_t* tokens, uint8_t* is_masked, int L, int B,
                   const uint8_t* role, const int32_t* b_len, const int32_t* t_lane,
                   int mode, float tau, int fallback_k, const int32_t* k_lane,
-                  const int32_t* delim_ids, int n_delim, int eos_id,
+                  const int32_t* delim_ids, int n_delim,
+                  const int32_t* digit_ids, int n_digit, const int32_t* open_ids, int n_open,
+                  const int32_t* close_ids, int n_close, int eos_id,
                   float rho_min, int t_min, float tau_future,
                   uint8_t* unmask_flag, int32_t* unmasked_pos, int32_t* still_masked_pos,
                   int32_t* counts, int32_t* lane_stats, uint8_t* delim_flag,

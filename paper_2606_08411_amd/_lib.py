@@ -40,7 +40,8 @@ _SIGNATURES = {
     "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
                                _sz, _vp]),
     "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
-                           _vp, _vp, _i, _i, _f, _i, _f, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+                           _vp, _vp, _i, _vp, _i, _vp, _i, _vp, _i, _i, _f, _i, _f,
+                           _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
 }
 
 _lib = None
@@ -210,11 +211,13 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
 def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=None,
                   t_lane=None, mode=MODE_THRESHOLD, tau=0.9, fallback_k=0, k_lane=None,
                   delim_ids=(0, 1), eos_id=2, rho_min=0.5, t_min=2, tau_future=None,
-                  with_delim_flag=True, out=None):
+                  with_delim_flag=True, out=None, digit_ids=(), open_ids=(), close_ids=()):
     """Per-lane transfer, lookahead drafts (tau_future None = off) and
     write-back (tokens / is_masked updated in place), ordered compaction and
-    lane statistics.  Returns a dict of device tensors: unmask_flag,
-    unmasked_pos, still_masked_pos, counts, lane_stats, delim_flag."""
+    lane statistics with ValidBoundary id sets (digit_ids, open_ids,
+    close_ids; empty = every delimiter counts).  Returns a dict of device
+    tensors: unmask_flag, unmasked_pos, still_masked_pos, counts,
+    lane_stats, delim_flag."""
     lib = library()
     N = int(row_pos.shape[0])
     dev = tokens.device
@@ -223,6 +226,7 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
     t_lane_h = None if t_lane is None else _host_i32(t_lane, L, "t_lane")
     k_lane_h = None if k_lane is None else _host_i32(k_lane, L, "k_lane")
     delim_h = np.ascontiguousarray(np.asarray(delim_ids, dtype=np.int32))
+    sets = [np.ascontiguousarray(np.asarray(x, dtype=np.int32)) for x in (digit_ids, open_ids, close_ids)]
     if out is None:
         out = dict(
             unmask_flag=torch.empty(max(N, 1), dtype=torch.uint8, device=dev),
@@ -235,7 +239,10 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
         _ptr(conf) if N else None, _ptr(argmax) if N else None, _ptr(row_pos) if N else None, N,
         _ptr(tokens), _ptr(is_masked), L, B, _np_ptr(role_h), _np_ptr(b_len_h), _np_ptr(t_lane_h),
         int(mode), float(tau), int(fallback_k), _np_ptr(k_lane_h),
-        _np_ptr(delim_h) if len(delim_h) else None, len(delim_h), int(eos_id), float(rho_min),
+        _np_ptr(delim_h) if len(delim_h) else None, len(delim_h),
+        _np_ptr(sets[0]) if len(sets[0]) else None, len(sets[0]),
+        _np_ptr(sets[1]) if len(sets[1]) else None, len(sets[1]),
+        _np_ptr(sets[2]) if len(sets[2]) else None, len(sets[2]), int(eos_id), float(rho_min),
         int(t_min), float("inf") if tau_future is None else float(tau_future),
         _ptr(out["unmask_flag"]), _ptr(out["unmasked_pos"]),
         _ptr(out["still_masked_pos"]), _ptr(out["counts"]), _ptr(out["lane_stats"]),

@@ -122,7 +122,9 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx,
 int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_pos, int N,
                   int32_t* tokens, uint8_t* is_masked, int L, int B, const uint8_t* role,
                   const int32_t* b_len, const int32_t* t_lane, int mode, float tau, int fallback_k,
-                  const int32_t* k_lane, const int32_t* delim_ids, int n_delim, int eos_id,
+                  const int32_t* k_lane, const int32_t* delim_ids, int n_delim,
+                  const int32_t* digit_ids, int n_digit, const int32_t* open_ids, int n_open,
+                  const int32_t* close_ids, int n_close, int eos_id,
                   float rho_min, int t_min, float tau_future, uint8_t* unmask_flag,
                   int32_t* unmasked_pos,
                   int32_t* still_masked_pos, int32_t* counts, int32_t* lane_stats,
@@ -135,6 +137,11 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
     return AL_ERR_SHAPE;
   if (!tokens || !is_masked || !role || !counts || !lane_stats) return AL_ERR_NULL;
   if (n_delim > 0 && !delim_ids) return AL_ERR_NULL;
+  if (n_digit < 0 || n_digit > AL_MAX_BOUNDARY_IDS || n_open < 0 || n_open > AL_MAX_BOUNDARY_IDS ||
+      n_close < 0 || n_close > AL_MAX_BOUNDARY_IDS)
+    return AL_ERR_SHAPE;
+  if ((n_digit > 0 && !digit_ids) || (n_open > 0 && !open_ids) || (n_close > 0 && !close_ids))
+    return AL_ERR_NULL;
   if (mode == AL_MODE_TOPK && !k_lane) return AL_ERR_NULL;
   if (N > 0 && (!conf || !argmax || !row_pos || !unmask_flag || !unmasked_pos || !still_masked_pos))
     return AL_ERR_NULL;
@@ -155,6 +162,12 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
   h.t_min = t_min;
   h.n_delim = n_delim;
   for (int j = 0; j < n_delim; ++j) h.delim[j] = delim_ids[j];
+  h.n_digit = n_digit;
+  h.n_open = n_open;
+  h.n_close = n_close;
+  for (int j = 0; j < n_digit; ++j) h.digit[j] = digit_ids[j];
+  for (int j = 0; j < n_open; ++j) h.open[j] = open_ids[j];
+  for (int j = 0; j < n_close; ++j) h.close[j] = close_ids[j];
   for (int i = 0; i < L; ++i) {
     if (role[i] != AL_ROLE_GEN && role[i] != AL_ROLE_REF) return AL_ERR_SHAPE;
     h.role[i] = role[i];

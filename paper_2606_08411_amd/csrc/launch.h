@@ -31,10 +31,14 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N, 
 constexpr int kSelMaxPositions = 8192;
 constexpr int kSelMaxLanes = 64;
 constexpr int kSelMaxDelims = 16;
+constexpr int kSelMaxBoundaryIds = 32;
 struct SelHost {
   int L, B, N, mode, fallback_k, eos_id, t_min, n_delim;
   float tau, rho_min, tau_future;
   int32_t delim[kSelMaxDelims];
+  // ValidBoundary id sets (empty = always valid).
+  int n_digit, n_open, n_close;
+  int32_t digit[kSelMaxBoundaryIds], open[kSelMaxBoundaryIds], close[kSelMaxBoundaryIds];
   uint8_t role[kSelMaxLanes];
   int32_t b_len[kSelMaxLanes];
   int32_t t_lane[kSelMaxLanes];

@@ -192,24 +192,45 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     p.counts[1] = base_s;
   }
 
-  // Lane boundary statistics on the updated state: one wavefront per lane.
+  // Lane boundary statistics on the updated state: one wavefront per lane,
+  // 64 positions per pass.  ValidBoundary: the bracket depth of [0, i] is
+  // an inclusive wavefront prefix sum plus the depth carried from earlier
+  // passes; the numeric-period test reads position i-1.
+  auto in_set = [](int tk, const int32_t* set, int n) {
+    bool hit = false;
+    for (int j = 0; j < n; ++j) hit |= (tk == set[j]);
+    return hit;
+  };
   for (int ln = w; ln < L; ln += SEL_WAVES) {
     const int n = h.b_len[ln];
-    int last = -1, filled = 0, stop = n;
-    for (int i = lane; i < B; i += kWave) {
+    int last = -1, filled = 0, stop = n, carry = 0;
+    for (int i0 = 0; i0 < B; i0 += kWave) {
+      const int i = i0 + lane;
       const int pos = ln * B + i;
+      const bool in = i < n;
+      const bool m = in ? s_msk[pos] != 0 : true;
+      const int tk = in ? s_tok[pos] : 0;
+      int delta = 0;
+      if (in && !m) delta = in_set(tk, h.open, h.n_open) ? 1 : (in_set(tk, h.close, h.n_close) ? -1 : 0);
+      int depth = delta;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int v = __shfl_up(depth, o, kWave);
+        if (lane >= o) depth += v;
+      }
+      depth += carry;
+      carry = __shfl(depth, kWave - 1, kWave);
       bool isd = false;
-      if (i < n) {
-        const bool m = s_msk[pos] != 0;
-        const int tk = s_tok[pos];
+      if (in) {
         if (!m) {
           ++filled;
-          for (int j = 0; j < h.n_delim; ++j) isd |= (tk == h.delim[j]);
+          isd = in_set(tk, h.delim, h.n_delim) && depth <= 0;
+          if (isd && i > 0 && !s_msk[pos - 1] && in_set(s_tok[pos - 1], h.digit, h.n_digit)) isd = false;
         }
         if (isd) last = i;
         if (m || tk == h.eos_id) stop = min(stop, i);
       }
-      if (p.delim_flag) p.delim_flag[pos] = (uint8_t)isd;
+      if (p.delim_flag && i < B) p.delim_flag[pos] = (uint8_t)isd;
     }
     last = wave_max(last);
     filled = wave_sum(filled);

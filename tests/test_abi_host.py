@@ -86,15 +86,16 @@ def test_lmhead_validation(lib):
 
 
 def _sel(lib, L=2, B=8, N=4, mode=0, role=(0, 0), b_len=None, k_lane=None, tau=0.9,
-         tau_future=2.0):
+         tau_future=2.0, n_digit=0, digits=None):
     role = np.asarray(role, np.uint8)
     bl = None if b_len is None else np.asarray(b_len, np.int32)
     kl = None if k_lane is None else np.asarray(k_lane, np.int32)
+    dg = None if digits is None else np.asarray(digits, np.int32)
     delim = np.array([0, 1], np.int32)
     cp = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
     return lib.select_unmask(FAKE, FAKE, FAKE, N, FAKE, FAKE, L, B, cp(role), cp(bl), None, mode,
-                             tau, 0, cp(kl), cp(delim), 2, 2, 0.5, 2, tau_future, FAKE, FAKE,
-                             FAKE, FAKE, FAKE, None, None)
+                             tau, 0, cp(kl), cp(delim), 2, cp(dg), n_digit, None, 0, None, 0,
+                             2, 0.5, 2, tau_future, FAKE, FAKE, FAKE, FAKE, FAKE, None, None)
 
 
 def test_select_validation(lib):
@@ -106,3 +107,5 @@ def test_select_validation(lib):
     assert _sel(lib, b_len=(8, 9)) == -2
     assert _sel(lib, tau=float("nan")) == -2
     assert _sel(lib, tau_future=float("nan")) == -2
+    assert _sel(lib, n_digit=1) == -1                     # ids missing
+    assert _sel(lib, n_digit=33, digits=np.arange(33)) == -2

@@ -17,18 +17,20 @@ pytestmark = pytest.mark.gpu
 
 
 def _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, mode, tau, fb,
-              k_lane, delim=(0, 1), eos=2, rho=0.5, tmin=2, tau_future=None):
+              k_lane, delim=(0, 1), eos=2, rho=0.5, tmin=2, tau_future=None, sets=((), (), ())):
     import paper_2606_08411_amd as al
     tok_d = dev(tokens)
     msk_d = dev(is_masked)
     out = al.select_unmask(dev(conf), dev(arg), dev(row_pos), tok_d, msk_d, L, B, role, b_len,
-                           t_lane, mode, tau, fb, k_lane, delim, eos, rho, tmin, tau_future)
+                           t_lane, mode, tau, fb, k_lane, delim, eos, rho, tmin, tau_future,
+                           digit_ids=sets[0], open_ids=sets[1], close_ids=sets[2])
     torch.cuda.synchronize()
     ref = oracle.select.select_unmask(conf, arg, row_pos, tokens, is_masked, B, role,
                                       b_len if b_len is not None else np.full(L, B),
                                       t_lane if t_lane is not None else np.zeros(L, np.int32),
                                       mode, tau, fb, k_lane, delim, eos, rho, tmin,
-                                      tau_future=tau_future)
+                                      tau_future=tau_future, digit_ids=sets[0],
+                                      open_ids=sets[1], close_ids=sets[2])
     N = len(row_pos)
     cu, cs = out["counts"].cpu().numpy()
     assert [cu, cs] == list(ref["counts"])
@@ -100,6 +102,37 @@ def test_select_lookahead_workloads(name, step_cache):
         ref = _run_both(conf, arg, s.row_pos, s.tokens, s.is_masked, s.L, s.B, s.role, b_len,
                         s.t_lane, 0, s.tau, 1, None, tau_future=tf)
     assert (ref["unmask_flag"] == 2).any()
+
+
+def test_select_valid_boundary():
+    """ValidBoundary id sets on random states, including lanes longer than
+    one wavefront pass (B up to 200), so the bracket depth carries across
+    passes."""
+    rng = np.random.default_rng(41)
+    sets_list = [((3, 4, 5), (), ()), ((), (6,), (7,)), ((3, 4), (6, 8), (7, 9)),
+                 (tuple(range(10, 42)), tuple(range(42, 74)), tuple(range(74, 106)))]
+    hits = 0
+    for trial in range(24):
+        L = int(rng.integers(1, 9))
+        B = int(rng.choice([8, 32, 64, 65, 128, 200]))
+        LB = L * B
+        is_masked = (rng.random(LB) < 0.25).astype(np.uint8)
+        row_pos = np.flatnonzero(rng.random(LB) < 0.5).astype(np.int32)
+        N = len(row_pos)
+        conf = rng.random(N).astype(np.float32)
+        hi = 12 if trial % 4 != 3 else 110
+        arg = rng.integers(0, hi, N).astype(np.int32)
+        tokens = rng.integers(0, hi, LB).astype(np.int32)
+        b_len = rng.integers(0, B + 1, L).astype(np.int32)
+        role = np.zeros(L, np.uint8)
+        t_lane = np.full(L, 3, np.int32)
+        sets = sets_list[trial % 4]
+        ref = _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, 0, 0.7,
+                        1, None, (0, 1), 2, 0.25, 2, None, sets)
+        plain = oracle.select.select_unmask(conf, arg, row_pos, tokens, is_masked, B, role, b_len,
+                                            t_lane, 0, 0.7, 1, None, (0, 1), 2, 0.25, 2)
+        hits += int((ref["delim_flag"] != plain["delim_flag"]).sum())
+    assert hits > 0   # the sets removed delimiters somewhere
 
 
 def test_select_empty_and_full():
