@@ -16,9 +16,11 @@ attention   lane-batched bidirectional attention over a shared prefix cache,
 lmhead      hidden->vocab logits, max-probability confidence and argmax, in a
             full-softmax form and a chunked online form (Section 3.2, the
             confidence-based transfer rule; refine-lane EOS suppression).
+refresh     the compact refresh window length (Section 3.4 "Compact cache
+            refresh and reuse").
 select      per-lane confidence-threshold / top-k transfer and the lane
             boundary statistics: split point (eq. split_point), fill ratio
             and step condition (eq. fork_condition), valid prefix length
             (Section 3.2 "Advancement control").
 """
-from . import attention, lmhead, select  # noqa: F401
+from . import attention, lmhead, refresh, select  # noqa: F401

@@ -735,3 +735,46 @@ SELECT_CHECKS = [check_select_brute_force, check_select_threshold_extremes,
                  check_lane_stats_golden, check_lane_stats_scan,
                  check_lookahead_golden, check_lookahead_properties,
                  check_valid_boundary_golden, check_valid_boundary_properties]
+
+
+# ------------------------------------------------------------------ refresh
+# Hand-worked L_refresh = min(P + L, P + max(s + v) + m) (Section 3.4).
+REFRESH_CASES = [
+    # P, L, lane starts, valid lengths, margin -> L_refresh
+    (100, 256, [0, 32, 64], [32, 10, 0], 16, 180),   # L_eff = max(32, 42, 64) = 64
+    (100, 256, [0, 32, 64], [32, 10, 0], 200, 356),  # margin runs past the end: P + L
+    (512, 128, [0], [0], 0, 512),                    # nothing valid yet: the prompt only
+    (512, 128, [], [], 8, 520),                      # no lanes: L_eff = 0
+    (7, 64, [40, 8], [24, 50], 3, 71),               # L_eff = max(64, 58) = 64 -> 7+64+3 = 74 > 71
+    (0, 64, [16, 0], [16, 8], 4, 36),                # no prompt: 0 + 32 + 4
+]
+
+
+def check_refresh_window_golden(rf):
+    for P, L, s, v, m, want in REFRESH_CASES:
+        assert rf.refresh_window_len(P, L, s, v, m) == want, (P, L, s, v, m)
+
+
+def check_refresh_window_properties(rf):
+    """P <= L_refresh <= P + L; monotone in the margin and in every lane's
+    frontier; independent of lane order."""
+    rng = np.random.default_rng(3)
+    for _ in range(200):
+        P = int(rng.integers(0, 600))
+        L = int(rng.integers(1, 1025))
+        n = int(rng.integers(0, 9))
+        s = rng.integers(0, L, n)
+        v = np.array([int(rng.integers(0, L - x + 1)) for x in s], dtype=np.int64)
+        m = int(rng.integers(0, 64))
+        r = rf.refresh_window_len(P, L, s, v, m)
+        assert P <= r <= P + L
+        assert rf.refresh_window_len(P, L, s, v, m + 1) >= r
+        perm = rng.permutation(n)
+        assert rf.refresh_window_len(P, L, s[perm], v[perm], m) == r
+        if n:
+            v2 = v.copy()
+            v2[0] = min(v2[0] + 5, L - s[0])
+            assert rf.refresh_window_len(P, L, s, v2, m) >= r
+
+
+REFRESH_CHECKS = [check_refresh_window_golden, check_refresh_window_properties]

@@ -84,10 +84,18 @@ MUTANTS = {
         ("close brackets ignored", "depth -= 1", "depth -= 0"),
         ("ValidBoundary ignored", "if tok in dset and valid_boundary(", "if tok in dset and True or valid_boundary("),
     ],
+    "refresh": [
+        ("margin dropped", "int(P) + l_eff + int(margin))", "int(P) + l_eff)"),
+        ("no clip at the sequence end", "return min(int(P) + int(L), int(P) + l_eff + int(margin))",
+         "return int(P) + l_eff + int(margin)"),
+        ("frontier without the lane start", "l_eff = max(l_eff, int(s) + int(v))", "l_eff = max(l_eff, int(v))"),
+        ("first lane only", "l_eff = max(l_eff, int(s) + int(v))", "l_eff = l_eff or int(s) + int(v)"),
+        ("prompt left out", "int(P) + l_eff + int(margin))", "l_eff + int(margin))"),
+    ],
 }
 
 CHECKS = {"attention": pins.ATTENTION_CHECKS, "lmhead": pins.LMHEAD_CHECKS,
-          "select": pins.SELECT_CHECKS}
+          "select": pins.SELECT_CHECKS, "refresh": pins.REFRESH_CHECKS}
 
 
 def _mutated(module, old, new):

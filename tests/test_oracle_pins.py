@@ -18,3 +18,8 @@ def test_lmhead_pin(check):
 @pytest.mark.parametrize("check", pins.SELECT_CHECKS, ids=lambda f: f.__name__)
 def test_select_pin(check):
     check(oracle.select)
+
+
+@pytest.mark.parametrize("check", pins.REFRESH_CHECKS, ids=lambda f: f.__name__)
+def test_refresh_pin(check):
+    check(oracle.refresh)
