@@ -107,6 +107,11 @@ const char* al_status_string(int status);
  * then computes the lanes over the updated prefix, and computes the
  * refreshed rows' queries q_ref over all P rows of the updated prefix only.
  *
+ * Compact cache refresh (Section 3.4): with L = 0 and n_refresh > 0 the call
+ * only refreshes.  Passing the window [0, L_refresh) as the prefix
+ * (P = L_refresh, see al_refresh_window) with refresh_idx = 0..P-1 is the
+ * bidirectional refresh forward over the window.
+ *
  * q        dev  [L*B][Hq][D]   lane query rows, lane-major (row = i*B + a)
  * k_lane   dev  [L*B][Hkv][D]  lane block keys (same row order)
  * v_lane   dev  [L*B][Hkv][D]
@@ -114,7 +119,9 @@ const char* al_status_string(int status);
  * v_prefix dev  [P][Hkv][D]
  * parent   host [L]            parent lane, -1 for a lane attached directly
  *                              to the prefix; parent[i] must be < i
- * L        1..AL_MAX_LANES;  B: 16..1024, multiple of 16;  P >= 0
+ * L        0..AL_MAX_LANES (0 only with n_refresh > 0: q, k_lane, v_lane,
+ *          parent, o, lse may then be NULL and B is ignored);
+ *          B: 16..1024, multiple of 16;  P >= 0
  * Hq, Hkv  Hq % Hkv == 0, Hq/Hkv <= 16;  D: 64 or 128
  * scale    softmax scale; <= 0 selects 1/sqrt(D)
  * refresh_idx dev [n_refresh] int32, unique rows in [0, P); n_refresh >= 0
@@ -244,6 +251,24 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
                   uint8_t* unmask_flag, int32_t* unmasked_pos, int32_t* still_masked_pos,
                   int32_t* counts, int32_t* lane_stats, uint8_t* delim_flag,
                   void* stream);
+
+/* ------------------------------------------------------------------------
+ * al_refresh_window -- length of the compact cache refresh window.
+ *
+ * Defined by Section 3.4 ("Compact cache refresh and reuse"):
+ *     L_refresh = min(P + L_gen, P + L_eff + margin),
+ *     L_eff = max over lanes of (lane_start[i] + valid_len[i])   (0 if none)
+ * P is the prompt length, L_gen the generation length, lane_start the
+ * lanes' starts and valid_len their valid prefix lengths (the
+ * AL_STAT_VALID column of select_unmask) in generation coordinates.
+ *
+ * lane_start, valid_len  host [n_lanes] int32 (>= 0), read during the call
+ * Returns L_refresh (>= 0) or a negative status: AL_ERR_SHAPE for a
+ * negative argument or a result above INT32_MAX, AL_ERR_NULL for missing
+ * arrays.  Host computation only; no device work.
+ * ------------------------------------------------------------------------ */
+int al_refresh_window(int P, int L_gen, const int32_t* lane_start, const int32_t* valid_len,
+                      int n_lanes, int margin);
 
 #ifdef __cplusplus
 }

@@ -6,14 +6,18 @@ Three calls, backed by hand-written HIP kernels in libasynclane.so:
   over a lane tree, with compact-refresh prefix rows (paper Sections 3.2, 3.4)
 * ``lmhead_confidence``  fused LM-head GEMM + online softmax: per masked
   position the max probability and its token, logits never stored
-* ``select_unmask``      per-lane threshold / top-k transfer, write-back and
-  lane boundary statistics (eq. split_point, eq. fork_condition)
+* ``select_unmask``      per-lane threshold / top-k transfer, lookahead
+  drafts, write-back and lane boundary statistics (eq. split_point,
+  eq. fork_condition, ValidBoundary)
+* ``al_refresh_window``  the compact cache refresh window length (Section
+  3.4); the refresh forward itself is a refresh-only ``lane_attn_forward``
 
 The functions are thin ctypes wrappers (see ``_lib``); they raise when the
 library has not been built (``python -m paper_2606_08411_amd.build``).
 """
 from ._lib import (  # noqa: F401
     AsyncLaneError,
+    al_refresh_window,
     LANE_STATS,
     MODE_THRESHOLD,
     MODE_TOPK,

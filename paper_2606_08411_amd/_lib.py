@@ -37,6 +37,7 @@ _SIGNATURES = {
     "lane_attn_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f,
                                _vp, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "lmhead_confidence_workspace_size": (_sz, [_i, _i, _i]),
+    "al_refresh_window": (_i, [_i, _i, _vp, _vp, _i, _i]),
     "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
                                _sz, _vp]),
     "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
@@ -139,19 +140,24 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
     q [L*B][Hq][D], k_lane/v_lane [L*B][Hkv][D], k_prefix/v_prefix
     [P][Hkv][D] are bf16 device tensors; parent is a host sequence of L ints.
     k_prefix / v_prefix are updated in place when refresh rows are given.
-    Returns (o, lse, o_ref, lse_ref)."""
+    A refresh-only call (compact cache refresh) passes q = k_lane = v_lane
+    = None and parent = [] with refresh rows.  Returns (o, lse, o_ref,
+    lse_ref)."""
     lib = library()
-    LB, Hq, D = q.shape
-    Hkv = k_lane.shape[1]
-    P = k_prefix.shape[0]
+    P, Hkv, D = k_prefix.shape
     L = len(parent)
     par = _host_i32(parent, L, "parent")
     n_ref = 0 if refresh_idx is None else int(refresh_idx.shape[0])
-    dev = q.device
-    if o is None:
-        o = torch.empty_like(q)
-    if lse is None and want_lse:
-        lse = torch.empty((LB, Hq), dtype=torch.float32, device=dev)
+    dev = k_prefix.device
+    if L > 0:
+        LB, Hq, _ = q.shape
+        if o is None:
+            o = torch.empty_like(q)
+        if lse is None and want_lse:
+            lse = torch.empty((LB, Hq), dtype=torch.float32, device=dev)
+    else:
+        Hq = q_ref.shape[1]
+        B = 16
     if n_ref:
         if o_ref is None:
             o_ref = torch.empty_like(q_ref)
@@ -163,7 +169,8 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
     else:
         ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
     st = lib.lane_attn_forward(
-        _ptr(q), _ptr(k_lane), _ptr(v_lane), _ptr(k_prefix), _ptr(v_prefix), _np_ptr(par),
+        _ptr(q), _ptr(k_lane), _ptr(v_lane), _ptr(k_prefix), _ptr(v_prefix),
+        _np_ptr(par) if L else None,
         L, B, P, Hq, Hkv, D, float(scale),
         _ptr(refresh_idx) if n_ref else None, n_ref,
         _ptr(q_ref) if n_ref else None, _ptr(k_ref) if n_ref else None,
@@ -171,6 +178,18 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
         _ptr(lse_ref) if n_ref else None, _ptr(o), _ptr(lse), _ptr(ws), ws_bytes, _stream())
     _check(st, "lane_attn_forward")
     return o, lse, o_ref, lse_ref
+
+
+def al_refresh_window(P, L_gen, lane_start, valid_len, margin) -> int:
+    """Compact refresh window length L_refresh (host computation)."""
+    n = len(lane_start)
+    s = _host_i32(lane_start, n, "lane_start")
+    v = _host_i32(valid_len, n, "valid_len")
+    r = int(library().al_refresh_window(int(P), int(L_gen), _np_ptr(s) if n else None,
+                                        _np_ptr(v) if n else None, n, int(margin)))
+    if r < 0:
+        _check(r, "al_refresh_window")
+    return r
 
 
 def lmhead_confidence_workspace_size(N, d, V) -> int:

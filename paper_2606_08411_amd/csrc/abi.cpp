@@ -44,8 +44,9 @@ const char* al_status_string(int status) {
 }
 
 static bool attn_shape_ok(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
-  if (L < 1 || L > AL_MAX_LANES) return false;
-  if (B < 16 || B > 1024 || B % 16 != 0) return false;
+  // L = 0 is a refresh-only call (compact cache refresh).
+  if (L < 0 || L > AL_MAX_LANES || (L == 0 && n_refresh == 0)) return false;
+  if (L > 0 && (B < 16 || B > 1024 || B % 16 != 0)) return false;
   if (P < 0 || n_refresh < 0 || n_refresh > P) return false;
   if (Hkv < 1 || Hq < Hkv || Hq % Hkv != 0 || Hq / Hkv > 16) return false;
   if (D != 64 && D != 128) return false;
@@ -64,13 +65,14 @@ int lane_attn_forward(const al_bf16* q, const al_bf16* k_lane, const al_bf16* v_
                       int n_refresh, const al_bf16* q_ref, const al_bf16* k_ref,
                       const al_bf16* v_ref, al_bf16* o_ref, float* lse_ref, al_bf16* o, float* lse,
                       void* workspace, size_t workspace_bytes, void* stream) {
-  if (!q || !k_lane || !v_lane || !parent || !o) return AL_ERR_NULL;
+  if (L > 0 && (!q || !k_lane || !v_lane || !parent || !o)) return AL_ERR_NULL;
   if (P > 0 && (!k_prefix || !v_prefix)) return AL_ERR_NULL;
   if (n_refresh > 0 && (!refresh_idx || !q_ref || !k_ref || !v_ref || !o_ref)) return AL_ERR_NULL;
   if (!attn_shape_ok(L, B, P, Hq, Hkv, D, n_refresh)) return AL_ERR_SHAPE;
   if (isnan(scale) || isinf(scale)) return AL_ERR_SHAPE;
-  if (!aligned16(q) || !aligned16(k_lane) || !aligned16(v_lane) || !aligned16(o) ||
-      (P > 0 && (!aligned16(k_prefix) || !aligned16(v_prefix))) || (lse && !aligned4(lse)))
+  if ((L > 0 && (!aligned16(q) || !aligned16(k_lane) || !aligned16(v_lane) || !aligned16(o) ||
+                 (lse && !aligned4(lse)))) ||
+      (P > 0 && (!aligned16(k_prefix) || !aligned16(v_prefix))))
     return AL_ERR_ALIGN;
   if (n_refresh > 0 && (!aligned16(q_ref) || !aligned16(k_ref) || !aligned16(v_ref) ||
                         !aligned16(o_ref) || !aligned4(refresh_idx) || (lse_ref && !aligned4(lse_ref))))
@@ -180,6 +182,22 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
   return hip_status(al::launch_select(h, conf, argmax, row_pos, tokens, is_masked, unmask_flag,
                                       unmasked_pos, still_masked_pos, counts, lane_stats,
                                       delim_flag, static_cast<hipStream_t>(stream)));
+}
+
+int al_refresh_window(int P, int L_gen, const int32_t* lane_start, const int32_t* valid_len,
+                      int n_lanes, int margin) {
+  if (P < 0 || L_gen < 0 || n_lanes < 0 || margin < 0) return AL_ERR_SHAPE;
+  if (n_lanes > 0 && (!lane_start || !valid_len)) return AL_ERR_NULL;
+  long long l_eff = 0;
+  for (int i = 0; i < n_lanes; ++i) {
+    if (lane_start[i] < 0 || valid_len[i] < 0) return AL_ERR_SHAPE;
+    const long long f = (long long)lane_start[i] + valid_len[i];
+    if (f > l_eff) l_eff = f;
+  }
+  const long long full = (long long)P + L_gen;
+  const long long win = (long long)P + l_eff + margin;
+  const long long r = win < full ? win : full;
+  return r > INT32_MAX ? AL_ERR_SHAPE : (int)r;
 }
 
 }  // extern "C"

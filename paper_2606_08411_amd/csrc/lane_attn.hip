@@ -422,7 +422,7 @@ AttnPlan attn_plan(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
   AttnPlan pl{};
   const int g = Hq / Hkv;
   const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
-  pl.n_split_lane = choose_split(a.base_wgs, a.total_key_tiles);
+  pl.n_split_lane = L > 0 ? choose_split(a.base_wgs, a.total_key_tiles) : 1;
   pl.ws_lane = pl.n_split_lane > 1 ? (size_t)pl.n_split_lane * L * B * Hq * (D + 2) * sizeof(float) : 0;
   pl.n_split_ref = 1;
   pl.ws_ref = 0;
@@ -495,9 +495,12 @@ hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, cons
   p.n_key_lanes = L;
   p.lane_key_tiles = (B + AT_KT - 1) / AT_KT;
   for (int i = 0; i < L; ++i) p.vis[i] = vis[i];
-  const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
-  hipError_t e = (D == 64) ? run_pass<64>(p, a, pl.n_split_lane, ws, stream)
-                           : run_pass<128>(p, a, pl.n_split_lane, ws, stream);
+  hipError_t e = hipSuccess;
+  if (L > 0) {  // L = 0: refresh-only call
+    const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
+    e = (D == 64) ? run_pass<64>(p, a, pl.n_split_lane, ws, stream)
+                  : run_pass<128>(p, a, pl.n_split_lane, ws, stream);
+  }
   if (e != hipSuccess || n_refresh <= 0) return e;
 
   // Refresh pass: refreshed rows over the updated prefix only.

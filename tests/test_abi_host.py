@@ -109,3 +109,33 @@ def test_select_validation(lib):
     assert _sel(lib, tau_future=float("nan")) == -2
     assert _sel(lib, n_digit=1) == -1                     # ids missing
     assert _sel(lib, n_digit=33, digits=np.arange(33)) == -2
+
+
+def test_refresh_window_host(lib):
+    """al_refresh_window is host code: it runs here, exactly against the
+    oracle's window rule, and rejects bad arguments."""
+    import oracle
+    rng = np.random.default_rng(5)
+    cp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    for _ in range(300):
+        P = int(rng.integers(0, 5000))
+        L = int(rng.integers(0, 3000))
+        n = int(rng.integers(0, 70))
+        s = rng.integers(0, max(L, 1), n).astype(np.int32)
+        v = rng.integers(0, 65, n).astype(np.int32)
+        m = int(rng.integers(0, 100))
+        got = lib.al_refresh_window(P, L, cp(s) if n else None, cp(v) if n else None, n, m)
+        assert got == oracle.refresh.refresh_window_len(P, L, s, v, m)
+    one = np.array([1], np.int32)
+    assert lib.al_refresh_window(-1, 10, None, None, 0, 0) == -2
+    assert lib.al_refresh_window(10, 10, None, None, 0, -1) == -2
+    assert lib.al_refresh_window(10, 10, None, cp(one), 1, 0) == -1
+    assert lib.al_refresh_window(10, 10, cp(-one), cp(one), 1, 0) == -2
+
+
+def test_refresh_only_attention_validation(lib):
+    f = lib.lane_attn_forward
+    # L = 0 without refresh rows is an error; with refresh rows lane pointers may be NULL
+    assert f(None, None, None, FAKE, FAKE, None, 0, 16, 64, 4, 4, 64, 0.0, None, 0, None, None,
+             None, None, None, None, None, None, 0, None) == -2
+    assert lib.lane_attn_workspace_size(0, 16, 64, 4, 4, 64, 0) == 0
