@@ -18,9 +18,11 @@ lmhead      hidden->vocab logits, max-probability confidence and argmax, in a
             confidence-based transfer rule; refine-lane EOS suppression).
 refresh     the compact refresh window length (Section 3.4 "Compact cache
             refresh and reuse").
+scheduler   the active-lane scheduler (Algorithm "AsyncLane active-lane
+            decoding": fork, spawn, stop, output reconstruction, NFE).
 select      per-lane confidence-threshold / top-k transfer and the lane
             boundary statistics: split point (eq. split_point), fill ratio
             and step condition (eq. fork_condition), valid prefix length
             (Section 3.2 "Advancement control").
 """
-from . import attention, lmhead, refresh, select  # noqa: F401
+from . import attention, lmhead, refresh, scheduler, select  # noqa: F401

@@ -778,3 +778,131 @@ def check_refresh_window_properties(rf):
 
 
 REFRESH_CHECKS = [check_refresh_window_golden, check_refresh_window_properties]
+
+
+# ------------------------------------------------------------------ scheduler
+def _script_conf(sc):
+    script = {(it, pos): (c, t) for it, pos, c, t in sc["script"]}
+    W = sc["B"] + sc["window"]
+
+    def conf_fn(it, order, lanes, rows):
+        conf, arg = [], []
+        for r in rows:
+            pos = lanes[order[r // W]].s + r % W
+            c, t = script.get((it, pos), (0.1, 20 + pos))
+            conf.append(c)
+            arg.append(t)
+        return np.array(conf, np.float32), np.array(arg, np.int32)
+    return conf_fn
+
+
+def _run_scenario(sch, sc, conf_fn=None):
+    return sch.run(sc["P"], sc["L"], sc["B"], sc["window"], conf_fn or _script_conf(sc),
+                   sc["max_iters"], tau=sc["tau"], fallback_k=sc["fallback_k"],
+                   tau_future=sc["tau_future"], rho_min=sc["rho_min"], t_min=sc["t_min"])
+
+
+def check_scheduler_golden(sch):
+    """Two hand-traced runs (tests/golden/scheduler_scenarios.json)."""
+    import json
+    G = json.load(open(os.path.join(GOLDEN, "scheduler_scenarios.json")))
+    assert len(G["scenarios"]) >= 2
+    for sc in G["scenarios"]:
+        S = _run_scenario(sch, sc)
+        lanes = [["gen" if ln.role == 0 else "ref", ln.s, ln.b, ln.kind, ln.v] for ln in S.lanes]
+        ex = sc["expect"]
+        assert lanes == ex["lanes"], (sc["name"], lanes)
+        assert S.collect() == ex["output"], (sc["name"], S.collect())
+        tk = [int(t) if not m else -1 for t, m in zip(S.tokens, S.masked)]
+        assert tk == ex["tokens"], (sc["name"], tk)
+        plans = [[[["gen" if S.lanes[x].role == 0 else "ref", S.lanes[x].s] for x in order], cp]
+                 for order, cp in S.plans if order]
+        assert plans == ex["plans"], (sc["name"], plans)
+        got = [S.iterations, S.nfe, S.forks, S.spawns, S.stops]
+        assert got == [ex[k] for k in ("iterations", "nfe", "forks", "spawns", "stops")], (sc["name"], got)
+
+
+def _random_conf(seed, p_delim=0.08, p_eos=0.02):
+    def conf_fn(it, order, lanes, rows):
+        rng = np.random.default_rng([seed, it])
+        n = len(rows)
+        conf = rng.uniform(0, 1, n).astype(np.float32)
+        arg = rng.integers(3, 50, n).astype(np.int32)
+        u = rng.random(n)
+        arg[u < p_delim] = rng.integers(0, 2, int((u < p_delim).sum()))
+        arg[(u >= p_delim) & (u < p_delim + p_eos)] = 2
+        return conf, arg
+    return conf_fn
+
+
+def check_scheduler_blockwise(sch):
+    """No delimiter ever predicted and no lookahead: no fork can happen, so
+    the lanes are the consecutive blocks [kB, (k+1)B) of block-wise
+    semi-autoregressive decoding (Section 3.1), one model call each
+    iteration, and the output is the whole sequence up to the first EOS."""
+    for seed in range(4):
+        L, B = 40, 8
+        cf = _random_conf(seed, p_delim=0.0, p_eos=0.0)
+        S = sch.run(0, L, B, 0, cf, 500, tau=0.7, fallback_k=1, t_min=1)
+        assert S.forks == 0
+        assert [(ln.s, ln.b, ln.role) for ln in S.lanes] == [(k * B, min(B, L - k * B), 0)
+                                                          for k in range((L + B - 1) // B)]
+        assert not S.masked.any()
+        assert S.collect() == [int(t) for t in S.tokens]
+        assert S.nfe == 1 + S.iterations
+
+
+def check_scheduler_structure(sch):
+    """Random runs: forks come from generate lanes and split them in place
+    (refine child at the parent's start, generate child right after it);
+    successors start at s + v; refine lanes have no children; a filled
+    position never changes afterwards; the output is a subsequence of the
+    final tokens in position order with no EOS from a generate leaf."""
+    for seed in range(6):
+        L, B, window = 48, 8, (0, 8)[seed % 2]
+        cf = _random_conf(seed)
+        S = sch.Scheduler(2, L, B, window)
+        seen = {}
+        for it in range(300):
+            order, _ = S.plan()
+            if not order:
+                break
+            tk, mk = S.blocks(order)
+            rows = np.flatnonzero(mk).astype(np.int32)
+            conf, arg = cf(it, order, S.lanes, rows)
+            ln = [S.lanes[x] for x in order]
+            res = __import__("oracle").select.select_unmask(
+                conf, arg, rows, tk, mk, S.W, np.array([x.role for x in ln], np.uint8),
+                np.array([x.b for x in ln], np.int32), np.array([x.t + 1 for x in ln], np.int32),
+                0, 0.8, 1, None, (0, 1), 2, 0.5, 2, tau_future=0.85 if window else None)
+            S.commit(order, res["tokens"], res["is_masked"], res["lane_stats"])
+            for pos in np.flatnonzero(S.masked == 0):
+                assert seen.setdefault(int(pos), int(S.tokens[pos])) == int(S.tokens[pos])
+        for ln in S.lanes:
+            kids = [S.lanes[c] for c in ln.children]
+            if ln.role == 1:
+                assert not kids
+            if ln.kind == "fork":
+                assert ln.role == 0 and kids[0].role == 1 and kids[0].s == ln.s
+                if len(kids) > 1:
+                    assert kids[1].role == 0 and kids[1].s == ln.s + kids[0].b
+            if ln.kind == "spawn":
+                assert len(kids) == 1 and kids[0].s == ln.s + ln.v and ln.v > 0
+            assert 0 <= ln.s and ln.s + ln.b <= L
+        out = S.collect()
+        it_tok = iter(int(t) for t in S.tokens)
+        assert all(any(x == y for y in it_tok) for x in out)   # subsequence
+        # NFE = 1 + sum over iterations of the prefix-state groups evaluated:
+        # the two children of a fork share one state, every other lane has
+        # its own (Section 3.4, shared-prefix lane batching).
+        nfe = 1
+        for order, _ in S.plans:
+            keys = set()
+            for x in order:
+                par = S.lanes[x].parent
+                keys.add(("fork", par) if par >= 0 and S.lanes[par].kind == "fork" else ("own", x))
+            nfe += len(keys)
+        assert S.nfe == nfe
+
+
+SCHEDULER_CHECKS = [check_scheduler_golden, check_scheduler_blockwise, check_scheduler_structure]

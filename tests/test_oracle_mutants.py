@@ -92,10 +92,27 @@ MUTANTS = {
         ("first lane only", "l_eff = max(l_eff, int(s) + int(v))", "l_eff = l_eff or int(s) + int(v)"),
         ("prompt left out", "int(P) + l_eff + int(margin))", "l_eff + int(margin))"),
     ],
+    "scheduler": [
+        ("generate child before refine child", "        self._dfs(0, order)\n",
+         "        self._dfs(0, order)\n        order = sorted(order, key=lambda x: self.lanes[x].role)\n"),
+        ("step count without the current step", "np.array([x.t + 1 for x in ln], np.int32)",
+         "np.array([x.t for x in ln], np.int32)"),
+        ("successor after the whole lane", "self._add(lid, GEN, ln.s + v, min(self.B, L - ln.s - v), g)",
+         "self._add(lid, GEN, ln.s + ln.b, min(self.B, L - ln.s - ln.b), g) if ln.s + ln.b < L else None"),
+        ("no cascade stop", "if v == 0 or ln.s + v >= L:", "if ln.s + v >= L:"),
+        ("EOS emitted", "if self.masked[pos] or (ln.role == GEN and self.tokens[pos] == eos_id):",
+         "if self.masked[pos]:"),
+        ("NFE counts lanes", "self.nfe += len(groups)", "self.nfe += len(order)"),
+        ("fork children share the parent group", "                g = self.next_group\n                self.next_group += 1\n                self._add(lid, REF",
+         "                g = ln.group\n                self._add(lid, REF"),
+        ("refine lanes spawn", "                if ln.role == GEN:\n                    v = int(st[sel.STAT_VALID])",
+         "                if True:\n                    v = int(st[sel.STAT_VALID])"),
+    ],
 }
 
 CHECKS = {"attention": pins.ATTENTION_CHECKS, "lmhead": pins.LMHEAD_CHECKS,
-          "select": pins.SELECT_CHECKS, "refresh": pins.REFRESH_CHECKS}
+          "select": pins.SELECT_CHECKS, "refresh": pins.REFRESH_CHECKS,
+          "scheduler": pins.SCHEDULER_CHECKS}
 
 
 def _mutated(module, old, new):
@@ -104,6 +121,7 @@ def _mutated(module, old, new):
     assert old in src, f"mutation anchor not found in oracle/{module}.py: {old!r}"
     mod = types.ModuleType(f"oracle_mutant_{module}")
     mod.__file__ = path
+    mod.__package__ = "oracle"      # relative imports resolve to the real oracle modules
     exec(compile(src.replace(old, new), path, "exec"), mod.__dict__)
     return mod
 

@@ -23,3 +23,8 @@ def test_select_pin(check):
 @pytest.mark.parametrize("check", pins.REFRESH_CHECKS, ids=lambda f: f.__name__)
 def test_refresh_pin(check):
     check(oracle.refresh)
+
+
+@pytest.mark.parametrize("check", pins.SCHEDULER_CHECKS, ids=lambda f: f.__name__)
+def test_scheduler_pin(check):
+    check(oracle.scheduler)
