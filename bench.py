@@ -44,6 +44,11 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-reps", type=int, default=50)
+    ap.add_argument("--decode", action="store_true",
+                    help="instead of the step benchmark, run whole synthetic decodes driven by "
+                         "the library's active-lane scheduler and print their JSON line")
+    ap.add_argument("--decode-len", type=int, default=256)
+    ap.add_argument("--decode-runs", type=int, default=3)
     return ap.parse_args()
 
 
@@ -140,12 +145,107 @@ def cpu_baseline(s):
     }
 
 
+def decode_bench(args):
+    """Whole decodes: the library scheduler (AlSched) plans each iteration,
+    one lane_attn_forward runs per prefix-state group, lmhead_confidence
+    scores the masked block rows, select_unmask transfers / drafts and
+    computes the lane statistics, and the scheduler commits (one host round
+    trip per iteration).  Synthetic model: seeded Q/K/V pools and hidden
+    rows; the workload's W with the delimiter rows scaled by 2.5 and the
+    EOS row by 1.8, so forks and cascade stops occur."""
+    import numpy as np
+    import torch
+
+    import paper_2606_08411_amd as al
+    import synth
+
+    s = synth.make_step(args.config, args.seed)
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng([args.seed, 77])
+    L, B, window = args.decode_len, s.B, s.B
+    Wb = B + window
+
+    def bf(a):
+        return torch.from_numpy(synth.f32_to_bf16_bits(np.asarray(a, np.float32)).view(np.int16)) \
+            .view(torch.bfloat16).to(dev)
+
+    W = torch.from_numpy(np.ascontiguousarray(s.W).view(np.int16)).view(torch.bfloat16).to(dev)
+    W[0:2] *= 2.5
+    W[2] *= 1.8
+    H = bf(rng.standard_normal((4 * L, s.d)) * rng.uniform(1, 6, (4 * L, 1)))
+    pool = lambda n, h: bf(rng.standard_normal((n, h, s.D)))
+    q, kl, vl = pool(64 * Wb, s.Hq), pool(64 * Wb, s.Hkv), pool(64 * Wb, s.Hkv)
+    kp, vp = pool(s.P + L, s.Hkv), pool(s.P + L, s.Hkv)
+
+    def one_decode():
+        S = al.AlSched(s.P, L, B, window, 64)
+        attn_calls = 0
+        for it in range(100000):
+            pl = S.plan()
+            n = len(pl["lane_id"])
+            if n == 0:
+                break
+            tk, mk = S.blocks()
+            for grp in sorted(set(pl["group"].tolist())):
+                idx = [k for k in range(n) if pl["group"][k] == grp]
+                parent = [idx.index(pl["call_parent"][k]) if pl["call_parent"][k] >= 0 else -1
+                          for k in idx]
+                Pg = s.P + int(min(pl["start"][k] for k in idx))
+                m = len(idx) * Wb
+                al.lane_attn_forward(q[:m], kl[:m], vl[:m], kp[:Pg], vp[:Pg], parent, Wb,
+                                     want_lse=False)
+                attn_calls += 1
+            rows = np.flatnonzero(mk).astype(np.int32)
+            glob = pl["start"][rows // Wb] + rows % Wb
+            row_idx = torch.from_numpy(((it % 4) * L + glob).astype(np.int32)).to(dev)
+            sup = torch.from_numpy((pl["role"][rows // Wb] == al.ROLE_REF).astype(np.uint8)).to(dev)
+            conf, arg, _ = al.lmhead_confidence(H, W, row_idx=row_idx, suppress_eos=sup,
+                                                eos_id=s.eos_id, want_lse=False)
+            tok_d = torch.from_numpy(tk).to(dev)
+            msk_d = torch.from_numpy(mk).to(dev)
+            out = al.select_unmask(conf, arg, torch.from_numpy(rows).to(dev), tok_d, msk_d, n, Wb,
+                                   pl["role"], pl["b_len"], pl["t_step"], al.MODE_THRESHOLD, s.tau,
+                                   1, None, s.delim_ids, s.eos_id, s.rho_min, s.t_min,
+                                   tau_future=s.tau, with_delim_flag=False)
+            S.commit(tok_d.cpu().numpy(), msk_d.cpu().numpy(), out["lane_stats"].cpu().numpy())
+        return S, attn_calls
+
+    one_decode()   # warm-up
+    torch.cuda.synchronize()
+    runs = []
+    for _ in range(args.decode_runs):
+        t0 = time.perf_counter()
+        S, calls = one_decode()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        runs.append((dt, S, calls))
+    dt = sorted(r[0] for r in runs)[len(runs) // 2]
+    S = runs[0][1]
+    c = S.counters()
+    n_out = len(S.collect(s.eos_id))
+    print(json.dumps({
+        "metric": "synthetic active-lane decode, committed tokens/s (scheduler + 3 device calls)",
+        "value": round(n_out / dt, 1), "unit": "tokens/s", "n_gpus": 1,
+        "higher_is_better": True, "data": "synthetic",
+        "config": {"workload": WORKLOAD_NAMES[args.config] + f"; decode of {L} positions, block "
+                   f"{B}, lookahead window {window}, delimiter rows of W x2.5, EOS row x1.8",
+                   "name": args.config, "seed": args.seed, "L_gen": L, "B": B, "window": window},
+        "ms_per_decode": round(dt * 1000, 3), "runs": args.decode_runs,
+        "iterations": c["iterations"], "nfe": c["nfe"], "forks": c["forks"],
+        "spawns": c["spawns"], "stops": c["stops"], "lanes": c["lanes"],
+        "committed_tokens": n_out, "ms_per_iteration": round(dt * 1000 / c["iterations"], 3),
+    }))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "this build has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
+    if args.decode:
+        decode_bench(args)
+        return
     import numpy as np
     import torch
 

@@ -270,6 +270,73 @@ int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_p
 int al_refresh_window(int P, int L_gen, const int32_t* lane_start, const int32_t* valid_len,
                       int n_lanes, int margin);
 
+/* ------------------------------------------------------------------------
+ * Active-lane scheduler (host) -- Section 3.3, the paper's active-lane
+ * decoding algorithm, with the fork operator (eq. fork_operator), the
+ * fork condition (eq. fork_condition, via select_unmask's lane_stats),
+ * cascading termination ("Advancement control"), output reconstruction and
+ * model-call NFE accounting (Section 3.4).
+ *
+ * Generation positions are 0..L_gen-1.  A lane has a role, a start s and a
+ * length b (its update region [s, s+b)); its block for select_unmask is the
+ * W = B + window positions [s, s+W) (region plus lookahead window; positions
+ * past L_gen are filled with pad_id).  One iteration:
+ *   n = al_sched_plan(...)            active lanes, depth-first, refine
+ *                                     children before generate children,
+ *                                     at most max_lanes
+ *   al_sched_blocks(...)              their [n][W] token / mask blocks
+ *   lane_attn_forward per group       (call_parent gives the in-call lane
+ *                                     tree), lmhead_confidence on the
+ *                                     masked rows, select_unmask with
+ *                                     L = n, B = W, b_len, role, t_lane =
+ *                                     t_step
+ *   al_sched_commit(...)              write-back (regions first, then
+ *                                     drafts into still-masked positions)
+ *                                     and transitions: a generate lane
+ *                                     with fork_ok forks at p = split into
+ *                                     refine (s, p) and generate (s+p,
+ *                                     min(B, L-s-p)) sharing a new group;
+ *                                     otherwise a filled lane completes and
+ *                                     a completed generate lane stops when
+ *                                     v = 0 or s+v >= L, else spawns a
+ *                                     generate successor at s+v (new group)
+ * NFE = 1 + sum over iterations of the number of groups evaluated.
+ *
+ * The scheduler object owns host memory only (created by al_sched_create,
+ * released by al_sched_destroy); every array argument is caller-owned host
+ * memory read or written during the call.  Not thread-safe per object.
+ * Errors: AL_ERR_NULL, AL_ERR_SHAPE (capacity too small, bad arguments).
+ * ------------------------------------------------------------------------ */
+typedef struct al_sched al_sched;
+
+/* NULL on bad arguments (P >= 0, L_gen >= 1, B >= 1, window >= 0,
+ * 1 <= max_lanes <= AL_MAX_LANES) or allocation failure. */
+al_sched* al_sched_create(int P, int L_gen, int B, int window, int max_lanes, int pad_id);
+void al_sched_destroy(al_sched* s);
+/* Next plan: returns n (0 = no active lane).  Per lane k < n: lane id,
+ * role (AL_ROLE_*), start, b_len, t_step (local steps including this one),
+ * group (prefix-state id) and call_parent (index in this plan of the lane
+ * whose block lane k sees -- its refine sibling -- or -1). */
+int al_sched_plan(al_sched* s, int32_t* lane_id, uint8_t* role, int32_t* start, int32_t* b_len,
+                  int32_t* t_step, int32_t* group, int32_t* call_parent, int cap);
+/* Blocks of the last plan: tokens [n][W] int32, masked [n][W] uint8. */
+int al_sched_blocks(const al_sched* s, int32_t* tokens, uint8_t* masked);
+/* Results of the last plan: blocks after select_unmask and its lane_stats
+ * [n][AL_LANE_STATS].  Returns the number of active lanes afterwards. */
+int al_sched_commit(al_sched* s, const int32_t* tokens, const uint8_t* masked,
+                    const int32_t* lane_stats);
+/* Output reconstruction into out [cap]; returns its length. */
+int al_sched_collect(const al_sched* s, int eos_id, int32_t* out, int cap);
+/* out [6]: iterations, nfe, forks, spawns, stops, lanes created. */
+int al_sched_counters(const al_sched* s, int32_t* out);
+/* Lane tree, lanes in creation order: role, start, length, parent (-1 for
+ * the root), kind (0 open/leaf, 1 forked, 2 spawned a successor) and v
+ * (valid length at spawn, else -1).  Returns the lane count. */
+int al_sched_tree(const al_sched* s, uint8_t* role, int32_t* start, int32_t* length,
+                  int32_t* parent, int32_t* kind, int32_t* v, int cap);
+/* Global generation state: tokens [L_gen] int32, masked [L_gen] uint8. */
+int al_sched_state(const al_sched* s, int32_t* tokens, uint8_t* masked);
+
 #ifdef __cplusplus
 }
 #endif

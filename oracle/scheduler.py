@@ -56,8 +56,9 @@ class Lane:
 
 
 class Scheduler:
-    def __init__(self, P, L, B, window=0, max_lanes=64):
+    def __init__(self, P, L, B, window=0, max_lanes=64, pad_id=3):
         self.P, self.L, self.B, self.window, self.max_lanes = P, L, B, window, max_lanes
+        self.pad_id = pad_id
         self.W = B + window
         self.tokens = np.full(L, -1, np.int32)
         self.masked = np.ones(L, np.uint8)
@@ -94,7 +95,7 @@ class Scheduler:
 
     def blocks(self, order):
         n, W = len(order), self.W
-        tk = np.full(n * W, 3, np.int32)      # padding past L: filled, id 3
+        tk = np.full(n * W, self.pad_id, np.int32)   # padding past L: filled
         mk = np.zeros(n * W, np.uint8)
         for i, lid in enumerate(order):
             s = self.lanes[lid].s

@@ -11,11 +11,14 @@ Three calls, backed by hand-written HIP kernels in libasynclane.so:
   eq. fork_condition, ValidBoundary)
 * ``al_refresh_window``  the compact cache refresh window length (Section
   3.4); the refresh forward itself is a refresh-only ``lane_attn_forward``
+* ``AlSched``            the host active-lane scheduler (Section 3.3) that
+  drives the three calls: plan, blocks, commit, collect
 
 The functions are thin ctypes wrappers (see ``_lib``); they raise when the
 library has not been built (``python -m paper_2606_08411_amd.build``).
 """
 from ._lib import (  # noqa: F401
+    AlSched,
     AsyncLaneError,
     al_refresh_window,
     LANE_STATS,

@@ -38,6 +38,15 @@ _SIGNATURES = {
                                _vp, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "lmhead_confidence_workspace_size": (_sz, [_i, _i, _i]),
     "al_refresh_window": (_i, [_i, _i, _vp, _vp, _i, _i]),
+    "al_sched_create": (_vp, [_i, _i, _i, _i, _i, _i]),
+    "al_sched_destroy": (None, [_vp]),
+    "al_sched_plan": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i]),
+    "al_sched_blocks": (_i, [_vp, _vp, _vp]),
+    "al_sched_commit": (_i, [_vp, _vp, _vp, _vp]),
+    "al_sched_collect": (_i, [_vp, _i, _vp, _i]),
+    "al_sched_counters": (_i, [_vp, _vp]),
+    "al_sched_tree": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i]),
+    "al_sched_state": (_i, [_vp, _vp, _vp]),
     "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
                                _sz, _vp]),
     "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
@@ -268,3 +277,82 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
         _ptr(out["delim_flag"]), _stream())
     _check(st, "select_unmask")
     return out
+
+
+# ------------------------------------------------------------------ scheduler
+class AlSched:
+    """Host active-lane scheduler (al_sched_* in include/asynclane.h); every
+    method is one call into the library.  Arrays are host numpy arrays."""
+
+    def __init__(self, P, L_gen, B, window=0, max_lanes=64, pad_id=3):
+        self._lib = library()
+        self.L, self.B, self.W = int(L_gen), int(B), int(B) + int(window)
+        self._h = self._lib.al_sched_create(int(P), int(L_gen), int(B), int(window),
+                                            int(max_lanes), int(pad_id))
+        if not self._h:
+            raise AsyncLaneError("al_sched_create: bad arguments")
+        self._n = 0
+
+    def __del__(self):
+        if getattr(self, "_h", None):
+            self._lib.al_sched_destroy(self._h)
+            self._h = None
+
+    def plan(self, cap=64):
+        """Returns dict of [n] arrays: lane_id, role, start, b_len, t_step,
+        group, call_parent."""
+        a = dict(lane_id=np.zeros(cap, np.int32), role=np.zeros(cap, np.uint8),
+                 start=np.zeros(cap, np.int32), b_len=np.zeros(cap, np.int32),
+                 t_step=np.zeros(cap, np.int32), group=np.zeros(cap, np.int32),
+                 call_parent=np.zeros(cap, np.int32))
+        n = self._lib.al_sched_plan(self._h, *[_np_ptr(a[k]) for k in
+                                              ("lane_id", "role", "start", "b_len", "t_step",
+                                               "group", "call_parent")], cap)
+        if n < 0:
+            _check(n, "al_sched_plan")
+        self._n = n
+        return {k: v[:n].copy() for k, v in a.items()}
+
+    def blocks(self):
+        tk = np.zeros(max(self._n, 1) * self.W, np.int32)
+        mk = np.zeros(max(self._n, 1) * self.W, np.uint8)
+        r = self._lib.al_sched_blocks(self._h, _np_ptr(tk), _np_ptr(mk))
+        if r < 0:
+            _check(r, "al_sched_blocks")
+        return tk[:self._n * self.W], mk[:self._n * self.W]
+
+    def commit(self, tokens, masked, lane_stats):
+        tk = np.ascontiguousarray(tokens, np.int32)
+        mk = np.ascontiguousarray(masked, np.uint8)
+        st = np.ascontiguousarray(lane_stats, np.int32)
+        r = self._lib.al_sched_commit(self._h, _np_ptr(tk), _np_ptr(mk), _np_ptr(st))
+        if r < 0:
+            _check(r, "al_sched_commit")
+        return r
+
+    def collect(self, eos_id=2):
+        out = np.zeros(self.L, np.int32)
+        n = self._lib.al_sched_collect(self._h, int(eos_id), _np_ptr(out), self.L)
+        if n < 0:
+            _check(n, "al_sched_collect")
+        return out[:n].tolist()
+
+    def counters(self):
+        out = np.zeros(6, np.int32)
+        _check(self._lib.al_sched_counters(self._h, _np_ptr(out)), "al_sched_counters")
+        return dict(zip(("iterations", "nfe", "forks", "spawns", "stops", "lanes"), out.tolist()))
+
+    def tree(self, cap=100000):
+        a = [np.zeros(cap, np.uint8)] + [np.zeros(cap, np.int32) for _ in range(5)]
+        n = self._lib.al_sched_tree(self._h, *[_np_ptr(x) for x in a], cap)
+        if n < 0:
+            _check(n, "al_sched_tree")
+        return dict(zip(("role", "start", "length", "parent", "kind", "v"), [x[:n].copy() for x in a]))
+
+    def state(self):
+        tk = np.zeros(self.L, np.int32)
+        mk = np.zeros(self.L, np.uint8)
+        r = self._lib.al_sched_state(self._h, _np_ptr(tk), _np_ptr(mk))
+        if r < 0:
+            _check(r, "al_sched_state")
+        return tk, mk

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libasynclane.so")
-SOURCES = ["abi.cpp", "lmhead.hip", "lane_attn.hip", "select_unmask.hip"]
+SOURCES = ["abi.cpp", "scheduler.cpp", "lmhead.hip", "lane_attn.hip", "select_unmask.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
