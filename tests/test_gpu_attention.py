@@ -94,6 +94,7 @@ SWEEP = [
     (128, 80, 4, "random", 8, 1, 1, 0.0),
     (64, 16, 12, "forest", 16, 2, 257, 0.3),
     (128, 32, 6, "linear", 28, 4, 130, 0.1),
+    (64, 1024, 2, "fork", 16, 1, 64, 0.0),      # largest block, largest GQA group
 ]
 
 

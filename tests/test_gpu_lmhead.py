@@ -57,6 +57,12 @@ SWEEP = [  # N, n_rows, d, V, eos
     (1, 1, 8, 1, -1), (1, 3, 8, 2, 1), (5, 9, 64, 7, 3), (33, 40, 264, 1000, 2),
     (100, 100, 128, 4097, 0), (130, 200, 520, 3000, 17), (300, 310, 64, 513, 2),
     (64, 64, 1024, 129, -1), (129, 150, 72, 777, 5),
+    # one case per fragment count / chunk size of the kernel: NF 3 ragged,
+    # NF 6 ragged (64-wide chunks), NF 7 plain, two NF-7 column tiles
+    # ragged, two NF-4 tiles with d < chunk, and V large enough (> 256
+    # tiles of 256 rows) for the CU-balanced vocab tiling
+    (77, 80, 200, 5000, 2), (190, 190, 136, 2048, 4), (224, 230, 256, 1500, -1),
+    (420, 450, 96, 700, 9), (225, 225, 64, 300, 1), (40, 40, 16, 70000, 3),
 ]
 
 
