@@ -8,6 +8,7 @@ namespace al {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
@@ -52,5 +53,17 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p) {
 // Lane exchange with lane l ^ 32 (the other half of the wavefront).
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, kWave); }
 __device__ __forceinline__ int xor32(int v) { return __shfl_xor(v, 32, kWave); }
+
+// max / sum of v over the lane pair (l, l ^ 32), the same value (and the
+// same bits: both operations commute) on both lanes.  One cross-half swap,
+// no LDS round trip.
+__device__ __forceinline__ float pair_max32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 }  // namespace al

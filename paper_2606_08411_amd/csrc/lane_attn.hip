@@ -206,7 +206,7 @@ void lane_attn_kernel(AttnParams p) {
       const int seg = tid + AT_THREADS * i;
       const int krow = seg / DSEG;
       const int ds = seg - krow * DSEG;
-      *reinterpret_cast<bf16x8*>(&k_s[krow * KSTR + ds * 8]) = krow < nvalid ? kr[i] : zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&k_s[krow * KSTR + ds * 8]) = (nvalid == AT_KT || krow < nvalid) ? kr[i] : zero_bf16x8();
     }
 #pragma unroll
     for (int i = 0; i < VREG; ++i) {
@@ -219,7 +219,7 @@ void lane_attn_kernel(AttnParams p) {
       const int pos = vt_pos4(k4);
       bf16x8 v4[4];
 #pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) v4[c4] = (4 * k4 + c4 < nvalid) ? vr[i][c4] : zero_bf16x8();
+      for (int c4 = 0; c4 < 4; ++c4) v4[c4] = (nvalid == AT_KT || 4 * k4 + c4 < nvalid) ? vr[i][c4] : zero_bf16x8();
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         bf16x4 col;
@@ -232,78 +232,105 @@ void lane_attn_kernel(AttnParams p) {
     }
   };
 
+  // One staged tile: S^T = K Q^T, the online softmax update in log2 units,
+  // then O^T += V^T P^T.  Only ragged tiles (nvalid < 64) mask; a 32-key
+  // half with no valid key is skipped in both products.
+  auto tile_compute = [&](int nvalid) {
+    const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
+    const f32x16 zero16 = {};
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      if (kb < nsub) {
+        sacc[kb] = zero16;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
+          sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sacc[kb][r] = -INFINITY;
+      }
+    }
+    if (nvalid < AT_KT) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          sacc[kb][r] = (key < nvalid) ? sacc[kb][r] : -INFINITY;
+        }
+    }
+    // The max is taken on the raw scores (the scale is positive, so
+    // max-then-scale is exact); each exponent is then one FMA.
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
+    mx = pair_max32(mx);
+    const float m_new = fmaxf(m_run, mx * p.scale_log2);
+    const float alpha = exp2_fast(m_run - m_new);
+    // P in bf16 (round-to-nearest-even, two values per conversion), packed
+    // per 16-key MFMA step; the row sum adds the rounded values (bf16 dot
+    // products with 1), so O is a convex combination of V rows.
+    float rs = 0.f;
+    bf16x8 pk[4];
+    const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int ks2 = 0; ks2 < 4; ++ks2)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const int r = 8 * (ks2 & 1) + e;
+        bf16x2 pr;
+        pr[0] = (__bf16)exp2_fast(fmaf(sacc[ks2 >> 1][r], p.scale_log2, -m_new));
+        pr[1] = (__bf16)exp2_fast(fmaf(sacc[ks2 >> 1][r + 1], p.scale_log2, -m_new));
+        pk[ks2][e] = pr[0];
+        pk[ks2][e + 1] = pr[1];
+        rs = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, rs, false);
+      }
+    rs = pair_sum32(rs);
+    l_run = l_run * alpha + rs;
+    m_run = m_new;
+    // Rescale O only when some row's max moved (otherwise alpha is exactly
+    // 1 and the product would change nothing).
+    if (__builtin_amdgcn_read_exec() & __ballot(alpha != 1.0f)) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+    }
+    // O^T += V^T P^T, one 16-key MFMA step at a time.
+#pragma unroll
+    for (int ks2 = 0; ks2 < 4; ++ks2) {
+      if ((ks2 >> 1) < nsub) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&vt_s[(dt * 32 + r32) * VSTR + ks2 * 16 + hh * 8]);
+          oacc[dt] = mfma32x32x16(a, pk[ks2], oacc[dt]);
+        }
+      }
+    }
+  };
+
   int kt = kt0;
   Tile cur = tile_at(kt);
   kt = next_kt(kt);
   if (cur.nvalid) load_tile(cur);
   while (cur.nvalid) {
     __syncthreads();  // the previous tile is no longer read
-    store_tile(cur.nvalid);
+    if (cur.nvalid == AT_KT)
+      store_tile(AT_KT);
+    else
+      store_tile(cur.nvalid);
     __syncthreads();
     // Prefetch the next visible tile while this one is multiplied.
     const Tile nxt = tile_at(kt);
     kt = next_kt(kt);
     if (nxt.nvalid) load_tile(nxt);
     if (cur.vis) {
-      const int nvalid = cur.nvalid;
-      const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
-      f32x16 sacc[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-        if (kb < nsub) {
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
-            sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
-          }
-        }
-      }
-      // Scale into log2 units, mask invalid keys, online softmax update.
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const float x = (key < nvalid) ? sacc[kb][r] * p.scale_log2 : -INFINITY;
-          sacc[kb][r] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, xor32(mx));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = exp2_fast(m_run - m_new);
-      // P in bf16 (round-to-nearest-even), packed per 16-key MFMA step;
-      // the row sum uses the rounded values so O is a convex combination.
-      float rs = 0.f;
-      bf16x8 pk[4];
-#pragma unroll
-      for (int ks2 = 0; ks2 < 4; ++ks2)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint16_t bits = f32_to_bf16_bits(exp2_fast(sacc[ks2 >> 1][8 * (ks2 & 1) + e] - m_new));
-          pk[ks2][e] = __builtin_bit_cast(__bf16, bits);
-          rs += bf16_bits_to_f32(bits);
-        }
-      rs += xor32(rs);
-      l_run = l_run * alpha + rs;
-      m_run = m_new;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
-      // O^T += V^T P^T, one 16-key MFMA step at a time.
-#pragma unroll
-      for (int ks2 = 0; ks2 < 4; ++ks2) {
-        if ((ks2 >> 1) < nsub) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(&vt_s[(dt * 32 + r32) * VSTR + ks2 * 16 + hh * 8]);
-            oacc[dt] = mfma32x32x16(a, pk[ks2], oacc[dt]);
-          }
-        }
-      }
+      tile_compute(cur.nvalid);
     }
     cur = nxt;
   }
@@ -317,10 +344,10 @@ void lane_attn_kernel(AttnParams p) {
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        uint16_t v4[4];
+        bf16x4 v4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = f32_to_bf16_bits(oacc[dt][rg * 4 + e] * inv_l);
-        *reinterpret_cast<uint2*>(op + dt * 32 + 8 * rg + 4 * hh) = __builtin_bit_cast(uint2, v4);
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)(oacc[dt][rg * 4 + e] * inv_l);
+        *reinterpret_cast<bf16x4*>(op + dt * 32 + 8 * rg + 4 * hh) = v4;
       }
     if (p.lse && hh == 0) p.lse[orow] = (m_run + log2f(l_run)) * AT_LN2;
   } else {
