@@ -11,7 +11,7 @@
 // d=4096) for a few tens to a few hundred hidden rows, so
 // lmhead_partial_kernel is shaped for HBM streaming first and MFMA reuse
 // second (measured on MI355X):
-// * each wavefront owns 32 vocabulary rows (the A operand of the 32x32x16
+// * each wavefront owns 32 or 64 vocabulary rows (A operands of the 32x32x16
 //   bf16 MFMA) and loads them straight into registers, two chunks ahead;
 //   each W element is used by one wavefront only;
 // * the chunk of the scored hidden rows (B operand, <= 224 rows per column
@@ -47,7 +47,7 @@ struct LmParams {
   const uint8_t* sup;
   LmPartial* part;  // [n_nt][nt_cols][n_vt]: a row's partials are contiguous
   int N, d, V, eos_id;
-  // Vocab tile vt covers rows [vt*V/n_vt, (vt+1)*V/n_vt) (<= 32*WAVES rows).
+  // Vocab tile vt covers rows [vt*V/n_vt, (vt+1)*V/n_vt) (<= 32*RT*WAVES rows).
   int n_vt, n_nt, nt_cols, tiles_total, tiles_per_xcd;
 };
 
@@ -68,8 +68,14 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
   m = M;
 }
 
-// WAVES wavefronts x 32 vocab rows per workgroup (VT = 32*WAVES), NF
+// WAVES wavefronts x 32*RT vocab rows per workgroup (VT = 32*RT*WAVES), NF
 // 32-column fragments (NT = 32*NF scored rows) per tile, 32x32x16 bf16 MFMA.
+// * RT = 2 (N <= 96): each wavefront owns two 32-row A tiles and uses every
+//   B fragment it reads from LDS for both, and a workgroup covers 512 vocab
+//   rows, so the hidden-chunk traffic per W byte halves.  Staging the hidden
+//   chunks was the main cost over a plain W stream (MI355X, LLaDA shape:
+//   186 µs with 32-row wavefronts, 177 µs with 64-row ones, 170 µs with no
+//   staging at all).
 // * W streams straight into registers, KC elements per chunk, PF chunks
 //   ahead (lane half h of row r takes K elements kc + 16s + 8h .. +8; over
 //   a chunk each row is read as one 2*KC-byte run).  Each W element is used
@@ -80,14 +86,14 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 //   prefetch, so the wait for them (the load counter is in-order) never
 //   waits for W loads that are still needed later.
 // * 32-row A tiles halve the B-operand LDS reads per FLOP of 16x16x32
-//   steps, and 256 vocab rows per workgroup keep the hidden-chunk traffic
-//   at NT/256 of the W traffic.
-// * Two wavefronts per SIMD: the accumulators take 16*NF registers.
-template <int NF, bool RAGGED, int WAVES, int KC, int PF>
+//   steps, and 256*RT vocab rows per workgroup keep the hidden-chunk
+//   traffic at NT/(256*RT) of the W traffic.
+// * Two wavefronts per SIMD: the accumulators take 16*NF*RT registers.
+template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
   constexpr int THREADS = WAVES * 64;
-  constexpr int VT = 32 * WAVES;                 // vocab rows per workgroup
+  constexpr int VT = 32 * RT * WAVES;            // vocab rows per workgroup
   constexpr int STEPS = KC / 16;                 // MFMA k-steps per chunk
   constexpr int NT = 32 * NF;                    // scored rows (columns) per tile
   constexpr int KSEG = KC / 8;                   // 16-byte segments per staged row
@@ -118,14 +124,15 @@ void lmhead_partial_kernel(LmParams p) {
   const int d = p.d;
   const int vb = (int)((long long)vt * p.V / p.n_vt);
   const int ve = (int)((long long)(vt + 1) * p.V / p.n_vt);
-  const int v0 = vb + w * 32;
+  const int v0 = vb + w * 32 * RT;
   const int n0 = nt * p.nt_cols;
   const int ncols = min(NT, p.N - n0);
 
   // Rows past the tile read its last row (cache hits; dropped in the
   // epilogue).
-  const uint16_t* wrow = p.W + (size_t)min(v0 + r32, ve - 1) * d;
-  const uint16_t* wlane = wrow + h * 8;
+  const uint16_t* wrow[RT];
+#pragma unroll
+  for (int q = 0; q < RT; ++q) wrow[q] = p.W + (size_t)min(v0 + 32 * q + r32, ve - 1) * d;
   unsigned hoff[HREG];
   int hcol[HREG];
   int hdst[HREG];
@@ -143,24 +150,26 @@ void lmhead_partial_kernel(LmParams p) {
     hvalid |= (ok ? 1u : 0u) << i;
   }
 
-  f32x16 acc[NF];
+  f32x16 acc[RT][NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f)
+  for (int q = 0; q < RT; ++q)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[f][r] = 0.f;
+    for (int f = 0; f < NF; ++f)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[q][f][r] = 0.f;
 
   constexpr int RING = PF + 1;   // W register slots (chunks)
-  bf16x8 wr[RING][STEPS], hr[2][HREG];
-  auto load_w1 = [&](int kc, int s) {
-    if (RAGGED) {
-      const int k = kc + s * 16 + h * 8;
-      return load_bf16x8(wrow + (k < d ? k : 0));
-    }
-    return load_bf16x8(wlane + kc + s * 16);
+  bf16x8 wr[RING][RT * STEPS], hr[2][HREG];
+  auto load_w1 = [&](int q, int kc, int s) {
+    const int k = kc + s * 16 + h * 8;
+    if (RAGGED) return load_bf16x8(wrow[q] + (k < d ? k : 0));
+    return load_bf16x8(wrow[q] + k);
   };
   auto load_w = [&](bf16x8* wv, int kc) {
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s) wv[s] = load_w1(kc, s);
+    for (int q = 0; q < RT; ++q)
+#pragma unroll
+      for (int s = 0; s < STEPS; ++s) wv[q * STEPS + s] = load_w1(q, kc, s);
   };
   auto load_h = [&](bf16x8* hv, int kh) {
 #pragma unroll
@@ -184,7 +193,8 @@ void lmhead_partial_kernel(LmParams p) {
 #pragma unroll
       for (int f = 0; f < NF; ++f) {
         const bf16x8 bv = *reinterpret_cast<const bf16x8*>(&buf[(f * 32 + r32) * STRIDE + s * 16 + h * 8]);
-        acc[f] = mfma32x32x16(wv[s], bv, acc[f]);
+#pragma unroll
+        for (int q = 0; q < RT; ++q) acc[q][f] = mfma32x32x16(wv[q * STEPS + s], bv, acc[q][f]);
       }
     }
   };
@@ -223,32 +233,34 @@ void lmhead_partial_kernel(LmParams p) {
     if (c + j < nch)
       chunk(c + j, wr[j % RING], wr[(j + PF) % RING], hr[(j + 1) & 1], hr[j & 1], false);
 
-  // Epilogue: lane (r32, h) holds vocab rows v0 + 8*(r/4) + 4h + r%4
-  // (r = 0..15) of column n0 + 32f + r32.
+  // Epilogue: lane (r32, h) holds vocab rows v0 + 32q + 8*(r/4) + 4h + r%4
+  // (q < RT, r = 0..15) of column n0 + 32f + r32.  Rows are visited in
+  // ascending order, so the first maximum is the lowest index.
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int n = n0 + f * 32 + r32;
     const bool sup_row = (n < p.N) && p.sup && p.sup[n];
+    // Branch-free: excluded rows become -inf, whose exponential is 0.
+    float z[RT][16];
     float m = -INFINITY;
     int idx = 0x7fffffff;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int v = v0 + 8 * (r >> 2) + 4 * h + (r & 3);
-      const bool ok = v < ve && !(sup_row && v == p.eos_id);
-      if (ok && acc[f][r] > m) {
-        m = acc[f][r];
-        idx = v;
-      }
-    }
-    float s = 0.f;
-    if (m != -INFINITY) {
+    for (int q = 0; q < RT; ++q)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int v = v0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const int v = v0 + 32 * q + 8 * (r >> 2) + 4 * h + (r & 3);
         const bool ok = v < ve && !(sup_row && v == p.eos_id);
-        if (ok) s += exp2_fast((acc[f][r] - m) * LM_LOG2E);
+        z[q][r] = ok ? acc[q][f][r] : -INFINITY;
+        const bool gt = z[q][r] > m;
+        m = gt ? z[q][r] : m;
+        idx = gt ? v : idx;
       }
-    }
+    const float m0 = (m == -INFINITY) ? 0.f : m;
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < RT; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s += exp2_fast((z[q][r] - m0) * LM_LOG2E);
     merge_state(m, s, idx, __shfl_xor(m, 32, kWave), __shfl_xor(s, 32, kWave),
                 __shfl_xor(idx, 32, kWave));
     if (h == 0) {
@@ -319,10 +331,13 @@ __global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
 
 // ------------------------------------------------------------------ host
 constexpr int LM_WAVES = 8;
-constexpr int LM_VT = 32 * LM_WAVES;
-// Chunk size per fragment count (no register spills at two wavefronts per
-// SIMD): 256-byte W runs up to 128 columns, 128-byte runs above.
-constexpr int lm_kc(int nf) { return nf <= 4 ? 128 : 64; }
+// Row tiles per wavefront and chunk size per fragment count (no register
+// spills at two wavefronts per SIMD): up to 96 columns two 32-row tiles
+// with 128-byte W runs; 128 columns one tile with 256-byte runs; above,
+// one tile with 128-byte runs.
+constexpr int lm_rt(int nf) { return nf <= 3 ? 2 : 1; }
+constexpr int lm_kc(int nf) { return nf == 4 ? 128 : 64; }
+constexpr int lm_vt(int nf) { return 32 * lm_rt(nf) * LM_WAVES; }
 constexpr int LM_PF = 2;
 
 // Column tiling: n_nt tiles of nf 32-column fragments (<= 224 columns).
@@ -352,11 +367,12 @@ static LmLayout lm_layout(int N, int V) {
   L.nf = N > 0 ? (frags + L.n_nt - 1) / L.n_nt : 1;
   L.nt_cols = 32 * L.nf;
   // One workgroup per CU runs at a time.  When the vocabulary needs more
-  // than one round of LM_VT-row tiles, the tile count is rounded up to a
+  // than one round of full tiles, the tile count is rounded up to a
   // multiple of the CU count and the rows are spread evenly, so the last
   // round is not partly empty (V = 152064: 594 full tiles would take 3
   // rounds at 77% use; 768 tiles of 198 rows take 3 even rounds).
-  const int base = (V + LM_VT - 1) / LM_VT;
+  const int vt_rows = lm_vt(L.nf);
+  const int base = (V + vt_rows - 1) / vt_rows;
   const int units = lm_cu_count();
   L.n_vt = base <= units ? base : units * ((base + units - 1) / units);
   L.total = sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
@@ -396,11 +412,11 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, lm_kc(F), LM_PF>), grid,   \
-                         block, 0, stream, p);                                                \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, lm_kc(F), LM_PF, lm_rt(F)>), \
+                         grid, block, 0, stream, p);                                          \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, lm_kc(F), LM_PF>), grid,  \
-                         block, 0, stream, p);                                                \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, lm_kc(F), LM_PF, lm_rt(F)>), \
+                         grid, block, 0, stream, p);                                          \
     break;
   switch (L.nf) {
     AL_LM_CASE(1)
