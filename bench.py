@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-reps", type=int, default=50)
+    ap.add_argument("--quick", action="store_true",
+                    help="skip the distribution, cold-input and graph passes (profiler runs)")
     ap.add_argument("--decode", action="store_true",
                     help="instead of the step benchmark, run whole synthetic decodes driven by "
                          "the library's active-lane scheduler and print their JSON line")
@@ -347,71 +349,83 @@ def main():
         torch.cuda.synchronize()
         return [a.elapsed_time(b) for a, b in evs]
 
-    # Distributions: whole steps (fresh selection state each), LM-head calls.
-    step_p = pct(per_rep(lambda k: step(nsteps + k), args.steps))
-    lm_p = pct(per_rep(lambda k: lm(), reps))
-    # The selection outcome of one step on fresh state (committed tokens).
-    n_commit = int(sel_out["counts"][0].item())
+    def extra_passes():
+        # Distributions: whole steps (fresh selection state each), LM-head calls.
+        step_p = pct(per_rep(lambda k: step(nsteps + k), args.steps))
+        lm_p = pct(per_rep(lambda k: lm(), reps))
+        # The selection outcome of one step on fresh state (committed tokens).
+        n_commit = int(sel_out["counts"][0].item())
 
-    # Cold attention: rotate over copies of the attention inputs whose total
-    # exceeds the 256 MB last-level cache, so no call finds its K/V cached.
-    set_bytes = sum(t.numel() * t.element_size() for t in (q, kl, vl, kp, vp))
-    n_sets = max(4, -(-512 * 2**20 // set_bytes))
-    sets = [tuple(t.clone() for t in (q, kl, vl, kp, vp)) for _ in range(n_sets)]
+        # Cold attention: rotate over copies of the attention inputs whose total
+        # exceeds the 256 MB last-level cache, so no call finds its K/V cached.
+        set_bytes = sum(t.numel() * t.element_size() for t in (q, kl, vl, kp, vp))
+        n_sets = max(4, -(-512 * 2**20 // set_bytes))
+        sets = [tuple(t.clone() for t in (q, kl, vl, kp, vp)) for _ in range(n_sets)]
 
-    def attn_set(k):
-        qq, kk, vv, kpp, vpp = sets[k % n_sets]
-        al.lane_attn_forward(qq, kk, vv, kpp, vpp, s.parent, s.B, o=o, lse=lse, o_ref=o_ref,
-                             lse_ref=lse_ref, **ref_args)
+        def attn_set(k):
+            qq, kk, vv, kpp, vpp = sets[k % n_sets]
+            al.lane_attn_forward(qq, kk, vv, kpp, vpp, s.parent, s.B, o=o, lse=lse, o_ref=o_ref,
+                                 lse_ref=lse_ref, **ref_args)
 
-    for k in range(n_sets):
-        attn_set(k)
-    it = iter(range(10**9))
-    t_attn_cold = timed(lambda: attn_set(next(it)), max(reps, 2 * n_sets))
-    del sets
+        for k in range(n_sets):
+            attn_set(k)
+        it = iter(range(10**9))
+        t_attn_cold = timed(lambda: attn_set(next(it)), max(reps, 2 * n_sets))
+        del sets
 
-    # HIP-graph replays (no host launch cost): the whole step, and each call
-    # captured 20 times in one graph.  The captured selection works on one
-    # (tokens, is_masked) pair, so later replays select on the evolving state.
-    graph = None
-    try:
-        tk_g, mk_g = toks[0].clone(), msks[0].clone()
-        sel_g = al.select_unmask(conf, arg, row_pos, tk_g, mk_g, s.L, s.B, s.role, s.b_len,
+        # HIP-graph replays (no host launch cost): the whole step, and each call
+        # captured 20 times in one graph.  The captured selection works on one
+        # (tokens, is_masked) pair, so later replays select on the evolving state.
+        graph = None
+        try:
+            tk_g, mk_g = toks[0].clone(), msks[0].clone()
+            sel_g = al.select_unmask(conf, arg, row_pos, tk_g, mk_g, s.L, s.B, s.role, s.b_len,
+                                     s.t_lane, al.MODE_THRESHOLD, s.tau, s.fallback_k,
+                                     delim_ids=s.delim_ids, eos_id=s.eos_id, rho_min=s.rho_min,
+                                     t_min=s.t_min)
+
+            def select_g():
+                al.select_unmask(conf, arg, row_pos, tk_g, mk_g, s.L, s.B, s.role, s.b_len,
                                  s.t_lane, al.MODE_THRESHOLD, s.tau, s.fallback_k,
                                  delim_ids=s.delim_ids, eos_id=s.eos_id, rho_min=s.rho_min,
-                                 t_min=s.t_min)
+                                 t_min=s.t_min, out=sel_g)
 
-        def select_g():
-            al.select_unmask(conf, arg, row_pos, tk_g, mk_g, s.L, s.B, s.role, s.b_len,
-                             s.t_lane, al.MODE_THRESHOLD, s.tau, s.fallback_k,
-                             delim_ids=s.delim_ids, eos_id=s.eos_id, rho_min=s.rho_min,
-                             t_min=s.t_min, out=sel_g)
+            def graph_ms(body, calls, n_rep):
+                g = torch.cuda.CUDAGraph()
+                torch.cuda.synchronize()
+                with torch.cuda.graph(g):
+                    for _ in range(calls):
+                        body()
+                for _ in range(3):
+                    g.replay()
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for _ in range(n_rep):
+                    g.replay()
+                b.record()
+                torch.cuda.synchronize()
+                return a.elapsed_time(b) / (n_rep * calls)
 
-        def graph_ms(body, calls, n_rep):
-            g = torch.cuda.CUDAGraph()
-            torch.cuda.synchronize()
-            with torch.cuda.graph(g):
-                for _ in range(calls):
-                    body()
-            for _ in range(3):
-                g.replay()
-            torch.cuda.synchronize()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            for _ in range(n_rep):
-                g.replay()
-            b.record()
-            torch.cuda.synchronize()
-            return a.elapsed_time(b) / (n_rep * calls)
-
-        graph = {
-            "ms_per_step": round(graph_ms(lambda: (attn(), lm(), select_g()), 1, args.steps), 4),
-            "per_call_ms": {"lane_attn_forward": round(graph_ms(attn, 20, 10), 4),
-                            "lmhead_confidence": round(graph_ms(lm, 5, 10), 4),
-                            "select_unmask": round(graph_ms(select_g, 20, 10), 4)},
+            graph = {
+                "ms_per_step": round(graph_ms(lambda: (attn(), lm(), select_g()), 1, args.steps), 4),
+                "per_call_ms": {"lane_attn_forward": round(graph_ms(attn, 20, 10), 4),
+                                "lmhead_confidence": round(graph_ms(lm, 5, 10), 4),
+                                "select_unmask": round(graph_ms(select_g, 20, 10), 4)},
+            }
+        except Exception as e:   # reported, never silent
+            graph = {"error": f"{type(e).__name__}: {e}"}
+        return {
+            "step_ms_p10_p50_p90": step_p,
+            "lmhead_ms_p10_p50_p90": lm_p,
+            "attention_cold_ms": round(t_attn_cold, 4),
+            "attention_cold_sets": n_sets,
+            "committed_tokens_per_step": n_commit,
+            "committed_tokens_per_s": round(n_commit / (ms_step * 1e-3), 1),
+            "graph": graph,
         }
-    except Exception as e:   # reported, never silent
-        graph = {"error": f"{type(e).__name__}: {e}"}
+
+    extras = extra_passes() if not args.quick else {}
 
     f_attn, f_lm = attention_flops(s), lmhead_flops(s)
     value = (f_attn + f_lm) / (ms_step * 1e-3) / 1e12
@@ -438,13 +452,7 @@ def main():
         "lane_tokens_per_s": round(s.L * s.B / (ms_step * 1e-3), 1),
         "per_call_ms": {"lane_attn_forward": round(t_attn, 4), "lmhead_confidence": round(t_lm, 4),
                         "select_unmask": round(t_sel, 4)},
-        "step_ms_p10_p50_p90": step_p,
-        "lmhead_ms_p10_p50_p90": lm_p,
-        "attention_cold_ms": round(t_attn_cold, 4),
-        "attention_cold_sets": n_sets,
-        "committed_tokens_per_step": n_commit,
-        "committed_tokens_per_s": round(n_commit / (ms_step * 1e-3), 1),
-        "graph": graph,
+        **extras,
         "attention_tflops": round(f_attn / (t_attn * 1e-3) / 1e12, 2),
         "lmhead_tflops": round(f_lm / (t_lm * 1e-3) / 1e12, 2),
         "roofline": {
