@@ -102,8 +102,7 @@ void lmhead_partial_kernel(LmParams p) {
   constexpr int STRIDE = KC + 8;
   constexpr int SEGS = NT * KSEG;
   constexpr int HREG = (SEGS + THREADS - 1) / THREADS;
-  constexpr int ROWS_STAGED = HREG * THREADS / KSEG;
-  constexpr int BUF = ROWS_STAGED * STRIDE;
+  constexpr int BUF = NT * STRIDE;
   __shared__ __attribute__((aligned(16))) uint16_t hs[2 * BUF];
   static_assert(sizeof(hs) >= 3 * sizeof(float) * WAVES * NT, "reduction scratch");
   float (*red_m)[NT] = reinterpret_cast<float (*)[NT]>(&hs[0]);
@@ -133,6 +132,10 @@ void lmhead_partial_kernel(LmParams p) {
   const uint16_t* wrow[RT];
 #pragma unroll
   for (int q = 0; q < RT; ++q) wrow[q] = p.W + (size_t)min(v0 + 32 * q + r32, ve - 1) * d;
+  // Hidden staging: segment i of this thread is row seg / KSEG of the
+  // column tile.  Only rows < ncols are loaded and stored each chunk; rows
+  // ncols..NT-1 (read by the MFMAs of the last fragment) are zeroed once in
+  // both buffers, and segments past NT rows do nothing.
   unsigned hoff[HREG];
   int hcol[HREG];
   int hdst[HREG];
@@ -143,11 +146,16 @@ void lmhead_partial_kernel(LmParams p) {
     const int row = seg / KSEG;
     const int k = (seg - row * KSEG) * 8;
     const bool ok = row < ncols;
+    const bool pad = !ok && row < NT;
     const int n = n0 + (ok ? row : 0);
     hoff[i] = (unsigned)(p.row_idx ? p.row_idx[n] : n) * (unsigned)d + (unsigned)k;
     hcol[i] = k;
-    hdst[i] = row * STRIDE + k;
+    hdst[i] = (row < NT ? row : 0) * STRIDE + k;
     hvalid |= (ok ? 1u : 0u) << i;
+    if (pad) {
+      *reinterpret_cast<bf16x8*>(&hs[hdst[i]]) = zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&hs[BUF + hdst[i]]) = zero_bf16x8();
+    }
   }
 
   f32x16 acc[RT][NF];
@@ -174,6 +182,7 @@ void lmhead_partial_kernel(LmParams p) {
   auto load_h = [&](bf16x8* hv, int kh) {
 #pragma unroll
     for (int i = 0; i < HREG; ++i) {
+      if (!((hvalid >> i) & 1u)) continue;
       if (RAGGED)
         hv[i] = load_bf16x8(p.hidden + (hcol[i] + kh < d ? hoff[i] + kh : hoff[i] - hcol[i]));
       else
@@ -183,8 +192,9 @@ void lmhead_partial_kernel(LmParams p) {
   auto store_h = [&](const bf16x8* hv, uint16_t* buf, int kh) {
 #pragma unroll
     for (int i = 0; i < HREG; ++i) {
+      if (!((hvalid >> i) & 1u)) continue;
       const bool kin = !RAGGED || hcol[i] + kh < d;
-      *reinterpret_cast<bf16x8*>(&buf[hdst[i]]) = (kin && ((hvalid >> i) & 1u)) ? hv[i] : zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&buf[hdst[i]]) = kin ? hv[i] : zero_bf16x8();
     }
   };
   auto mma = [&](const bf16x8* wv, const uint16_t* buf) {
