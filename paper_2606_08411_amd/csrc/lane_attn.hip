@@ -368,29 +368,39 @@ void lane_attn_kernel(AttnParams p) {
   }
 }
 
-// Combine the key splits of each (row, head): one wavefront per (row, head).
-template <int D>
+// Combine the NS key splits of each (row, head): one wavefront per (row,
+// head).  NS is a template argument so every split's loads issue at once
+// (one memory round trip); the splits are summed in ascending order.
+template <int D, int NS>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const float* part_o, const float* part_ml,
-                                                         int n_split, int n_rowheads,
-                                                         uint16_t* o, float* lse) {
+                                                         int n_rowheads, uint16_t* o, float* lse) {
   const int rh = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (rh >= n_rowheads) return;
-  float M = -INFINITY;
-  for (int s = 0; s < n_split; ++s) M = fmaxf(M, part_ml[((size_t)s * n_rowheads + rh) * 2]);
-  float L = 0.f;
   constexpr int PER = D / 64;
+  float m[NS], l[NS], po[NS][PER];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const float2 ml = *reinterpret_cast<const float2*>(part_ml + ((size_t)s * n_rowheads + rh) * 2);
+    m[s] = ml.x;
+    l[s] = ml.y;
+    const float* src = part_o + ((size_t)s * n_rowheads + rh) * D + lane * PER;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) po[s][e] = src[e];
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) M = fmaxf(M, m[s]);
+  float L = 0.f;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  for (int s = 0; s < n_split; ++s) {
-    const float m = part_ml[((size_t)s * n_rowheads + rh) * 2];
-    const float l = part_ml[((size_t)s * n_rowheads + rh) * 2 + 1];
-    const float wgt = (m == -INFINITY) ? 0.f : exp2_fast(m - M);
-    L += l * wgt;
-    const float* po = part_o + ((size_t)s * n_rowheads + rh) * D;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += po[lane * PER + e] * wgt;
+  for (int s = 0; s < NS; ++s) {
+    const float wgt = (m[s] == -INFINITY) ? 0.f : exp2_fast(m[s] - M);
+    L += l[s] * wgt;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] += po[s][e] * wgt;
   }
   const float inv = 1.0f / L;
 #pragma unroll
@@ -482,8 +492,23 @@ static hipError_t run_pass(const AttnParams& base, const PassShape& s, int n_spl
   hipLaunchKernelGGL(lane_attn_kernel<D>, grid, dim3(AT_THREADS), 0, stream, p);
   if (n_split > 1) {
     const int nrh = s.n_rows * p.Hq;
-    hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((nrh + 3) / 4), dim3(256), 0, stream, p.part_o,
-                       p.part_ml, n_split, nrh, p.o, p.lse);
+    const dim3 mgrid((nrh + 3) / 4), mblock(256);
+    switch (n_split) {  // choose_split returns a power of two <= 16
+      case 2:
+        hipLaunchKernelGGL((attn_merge_kernel<D, 2>), mgrid, mblock, 0, stream, p.part_o, p.part_ml, nrh, p.o, p.lse);
+        break;
+      case 4:
+        hipLaunchKernelGGL((attn_merge_kernel<D, 4>), mgrid, mblock, 0, stream, p.part_o, p.part_ml, nrh, p.o, p.lse);
+        break;
+      case 8:
+        hipLaunchKernelGGL((attn_merge_kernel<D, 8>), mgrid, mblock, 0, stream, p.part_o, p.part_ml, nrh, p.o, p.lse);
+        break;
+      case 16:
+        hipLaunchKernelGGL((attn_merge_kernel<D, 16>), mgrid, mblock, 0, stream, p.part_o, p.part_ml, nrh, p.o, p.lse);
+        break;
+      default:
+        return hipErrorInvalidValue;
+    }
   }
   return hipGetLastError();
 }
