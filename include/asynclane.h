@@ -191,7 +191,7 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
  * Defined by Section 3.2: the transfer rule is applied to each lane's valid
  * update region [0, b_len[l]) (refine lanes: the discovered prefix); the
  * transferred positions take their argmax token and are written back; then
- * the lane's split point (eq. split_point, ValidBoundary taken as true),
+ * the lane's split point (eq. split_point, with the ValidBoundary id sets below),
  * fill ratio and step condition (eq. fork_condition) and valid prefix length
  * ("Advancement control") are computed on the updated state.
  *
