@@ -50,6 +50,10 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const i32x4*>(p));
 }
 
+// s_waitcnt immediate for gfx9-family encodings: wait until at most n vector
+// memory loads are outstanding (n <= 63), no wait on the other counters.
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
 // Lane exchange with lane l ^ 32 (the other half of the wavefront).
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, kWave); }
 __device__ __forceinline__ int xor32(int v) { return __shfl_xor(v, 32, kWave); }

@@ -84,7 +84,7 @@ void lane_attn_kernel(AttnParams p) {
   const int split = blockIdx.z;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar registers and branches
   const int r32 = lane & 31;
   const int hh = lane >> 5;
   const int per_lane = p.tiles_per_lane * p.g;
@@ -317,7 +317,21 @@ void lane_attn_kernel(AttnParams p) {
   int kt = kt0;
   Tile cur = tile_at(kt);
   kt = next_kt(kt);
-  if (cur.nvalid) load_tile(cur);
+  {
+    // The first tile's loads are issued unconditionally (a split with no
+    // tile reads row 0 of Q instead, which always exists), so that straight
+    // after them one wait covers exactly the Q fragments.  Without it the
+    // compiler cannot tell at the loop header whether the Q loads are done
+    // and waits for every outstanding load before the first MFMA of each
+    // tile, which also waited for the next tile's prefetch.
+    Tile first = cur;
+    if (!first.nvalid) {
+      first.k = first.v = p.q;
+      first.nvalid = 1;
+    }
+    load_tile(first);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(KREG + 4 * VREG));
+  }
   while (cur.nvalid) {
     __syncthreads();  // the previous tile is no longer read
     if (cur.nvalid == AT_KT)
