@@ -95,6 +95,9 @@ SWEEP = [
     (64, 16, 12, "forest", 16, 2, 257, 0.3),
     (128, 32, 6, "linear", 28, 4, 130, 0.1),
     (64, 1024, 2, "fork", 16, 1, 64, 0.0),      # largest block, largest GQA group
+    (128, 32, 64, "forest", 4, 1, 0, 0.0),      # no prefix, 64 roots: many key splits
+                                                # hold no tile any wavefront of a
+                                                # workgroup sees (empty-split path)
 ]
 
 
