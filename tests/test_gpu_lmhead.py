@@ -57,12 +57,16 @@ SWEEP = [  # N, n_rows, d, V, eos
     (1, 1, 8, 1, -1), (1, 3, 8, 2, 1), (5, 9, 64, 7, 3), (33, 40, 264, 1000, 2),
     (100, 100, 128, 4097, 0), (130, 200, 520, 3000, 17), (300, 310, 64, 513, 2),
     (64, 64, 1024, 129, -1), (129, 150, 72, 777, 5),
-    # one case per fragment count / chunk size of the kernel: NF 3 ragged,
-    # NF 6 ragged (64-wide chunks), NF 7 plain, two NF-7 column tiles
-    # ragged, two NF-4 tiles with d < chunk, and V large enough (> 256
-    # tiles of 256 rows) for the CU-balanced vocab tiling
+    # kernel variants (64-element chunks; a d that is not a multiple of 64
+    # takes the ragged variant): NF 3 (two row tiles per wavefront) ragged,
+    # NF 6 ragged, NF 7 plain, two NF-7 column tiles ragged, two NF-4 tiles
+    # with d = one chunk, V large enough for the CU-balanced vocab tiling
+    # (two row tiles), then NF 4 (three chunks in flight): d below one
+    # chunk, plain over 7 chunks, ragged over 6, and the balanced tiling
     (77, 80, 200, 5000, 2), (190, 190, 136, 2048, 4), (224, 230, 256, 1500, -1),
     (420, 450, 96, 700, 9), (225, 225, 64, 300, 1), (40, 40, 16, 70000, 3),
+    (128, 130, 40, 900, 7), (100, 110, 448, 2000, 1), (120, 120, 328, 1200, 0),
+    (97, 100, 64, 70000, 3),
 ]
 
 
