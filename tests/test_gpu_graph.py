@@ -5,7 +5,9 @@ the graph holds the same launches).
 Between replays the test runs eager work of its own (a fresh eager step on
 other buffers) and synchronises; the selection state is reset by an eager
 copy before each replay, so every replay selects on the same input state.
-The graph holds kernel launches only (no memset nodes).
+The Wide workload includes the compact-refresh scatter, which rewrites the
+same prefix rows with the same values on every replay.  The graph holds
+kernel launches only (no memset nodes).
 """
 import numpy as np
 import pytest
@@ -75,7 +77,7 @@ class _Step:
         return [x.clone() for x in out]
 
 
-@pytest.mark.parametrize("name", ["tiny", "llada"])
+@pytest.mark.parametrize("name", ["tiny", "llada", "wide"])
 def test_graph_replays_match_eager(name):
     s, t = _inputs(name, 0)
     st = _Step(s, t)
