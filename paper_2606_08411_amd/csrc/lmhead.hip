@@ -30,7 +30,9 @@
 
 namespace al {
 
-constexpr int LM_MAX_NF = 7;     // <= 224 scored rows per column tile
+constexpr int LM_MAX_NF = 7;
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
+constexpr int lcm_c(int a, int b) { return a / gcd_c(a, b) * b; }     // <= 224 scored rows per column tile
 constexpr float LM_LOG2E = 1.4426950408889634f;
 
 struct LmPartial {
@@ -89,17 +91,18 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 //   steps, and 256*RT vocab rows per workgroup keep the hidden-chunk
 //   traffic at NT/(256*RT) of the W traffic.
 // * Two wavefronts per SIMD: the accumulators take 16*NF*RT registers.
-template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT>
+template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, int HD>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
   constexpr int THREADS = WAVES * 64;
   constexpr int VT = 32 * RT * WAVES;            // vocab rows per workgroup
   constexpr int STEPS = KC / 16;                 // MFMA k-steps per chunk
   constexpr int NT = 32 * NF;                    // scored rows (columns) per tile
-  constexpr int KSEG = KC / 8;                   // 16-byte segments per staged row
+  constexpr int KH = KC * SC;                    // K elements per staged hidden block
+  constexpr int KSEG = KH / 8;                   // 16-byte segments per staged row
   // +16 B per staged row: the 32 rows read by one half-wavefront start
   // 4 banks apart, so the B-operand reads are conflict-free.
-  constexpr int STRIDE = KC + 8;
+  constexpr int STRIDE = KH + 8;
   constexpr int SEGS = NT * KSEG;
   constexpr int HREG = (SEGS + THREADS - 1) / THREADS;
   constexpr int BUF = NT * STRIDE;
@@ -132,29 +135,27 @@ void lmhead_partial_kernel(LmParams p) {
   const uint16_t* wrow[RT];
 #pragma unroll
   for (int q = 0; q < RT; ++q) wrow[q] = p.W + (size_t)min(v0 + 32 * q + r32, ve - 1) * d;
-  // Hidden staging: segment i of this thread is row seg / KSEG of the
-  // column tile.  Only rows < ncols are loaded and stored each chunk; rows
-  // ncols..NT-1 (read by the MFMAs of the last fragment) are zeroed once in
-  // both buffers, and segments past NT rows do nothing.
+  // Hidden staging: segment i of this thread is row hrow0 + i * RSTEP of
+  // the column tile, at K offset hk of the staged block.  Only rows < ncols
+  // are loaded and stored each block; rows ncols..NT-1 (read by the MFMAs
+  // of the last fragment) are zeroed once in both buffers, and segments
+  // past NT rows do nothing.
+  static_assert(THREADS % KSEG == 0, "every segment of a thread has the same K offset");
+  constexpr int RSTEP = THREADS / KSEG;          // staged rows per segment round
+  const int hk = (tid % KSEG) * 8;               // this thread's K offset in a block
+  const int hrow0 = tid / KSEG;                  // segment i is row hrow0 + i * RSTEP
   unsigned hoff[HREG];
-  int hcol[HREG];
-  int hdst[HREG];
   unsigned hvalid = 0;
 #pragma unroll
   for (int i = 0; i < HREG; ++i) {
-    const int seg = tid + THREADS * i;
-    const int row = seg / KSEG;
-    const int k = (seg - row * KSEG) * 8;
+    const int row = hrow0 + i * RSTEP;
     const bool ok = row < ncols;
-    const bool pad = !ok && row < NT;
     const int n = n0 + (ok ? row : 0);
-    hoff[i] = (unsigned)(p.row_idx ? p.row_idx[n] : n) * (unsigned)d + (unsigned)k;
-    hcol[i] = k;
-    hdst[i] = (row < NT ? row : 0) * STRIDE + k;
+    hoff[i] = (unsigned)(p.row_idx ? p.row_idx[n] : n) * (unsigned)d + (unsigned)hk;
     hvalid |= (ok ? 1u : 0u) << i;
-    if (pad) {
-      *reinterpret_cast<bf16x8*>(&hs[hdst[i]]) = zero_bf16x8();
-      *reinterpret_cast<bf16x8*>(&hs[BUF + hdst[i]]) = zero_bf16x8();
+    if (!ok && row < NT) {
+      *reinterpret_cast<bf16x8*>(&hs[row * STRIDE + hk]) = zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&hs[BUF + row * STRIDE + hk]) = zero_bf16x8();
     }
   }
 
@@ -167,7 +168,7 @@ void lmhead_partial_kernel(LmParams p) {
       for (int r = 0; r < 16; ++r) acc[q][f][r] = 0.f;
 
   constexpr int RING = PF + 1;   // W register slots (chunks)
-  bf16x8 wr[RING][RT * STEPS], hr[2][HREG];
+  bf16x8 wr[RING][RT * STEPS], hr[HD][HREG];
   auto load_w1 = [&](int q, int kc, int s) {
     const int k = kc + s * 16 + h * 8;
     if (RAGGED) return load_bf16x8(wrow[q] + (k < d ? k : 0));
@@ -184,7 +185,7 @@ void lmhead_partial_kernel(LmParams p) {
     for (int i = 0; i < HREG; ++i) {
       if (!((hvalid >> i) & 1u)) continue;
       if (RAGGED)
-        hv[i] = load_bf16x8(p.hidden + (hcol[i] + kh < d ? hoff[i] + kh : hoff[i] - hcol[i]));
+        hv[i] = load_bf16x8(p.hidden + (hk + kh < d ? hoff[i] + kh : hoff[i] - hk));
       else
         hv[i] = load_bf16x8(p.hidden + (hoff[i] + kh));
     }
@@ -193,8 +194,8 @@ void lmhead_partial_kernel(LmParams p) {
 #pragma unroll
     for (int i = 0; i < HREG; ++i) {
       if (!((hvalid >> i) & 1u)) continue;
-      const bool kin = !RAGGED || hcol[i] + kh < d;
-      *reinterpret_cast<bf16x8*>(&buf[hdst[i]]) = kin ? hv[i] : zero_bf16x8();
+      const bool kin = !RAGGED || hk + kh < d;
+      *reinterpret_cast<bf16x8*>(&buf[(hrow0 + i * RSTEP) * STRIDE + hk]) = kin ? hv[i] : zero_bf16x8();
     }
   };
   auto mma = [&](const bf16x8* wv, const uint16_t* buf) {
@@ -209,39 +210,53 @@ void lmhead_partial_kernel(LmParams p) {
     }
   };
 
-  // Chunk c: W in register slot c % RING, hidden chunk in LDS buffer
-  // c % 2, hidden registers hr[c % 2] receive chunk c+2.
+  // Chunk c (KC columns of K): W in register slot c % RING.  The hidden
+  // rows are staged SC chunks at a time: block s (chunks s*SC ..) sits in
+  // LDS buffer s % 2, and a ring of HD register slots holds blocks s + 1
+  // .. s + HD in flight.  At the end of block s, block s + 1 is stored (the
+  // only barrier follows) and its slot is refilled with block s + 1 + HD.
+  // For N > 96, larger blocks (SC = 2, one slot) cost less than one per
+  // chunk (MI355X: Dream 279 -> 270 us, Long 301 -> 292 us, Wide 771 -> 735
+  // us per call); the 64-row kernels (N <= 96) keep SC = 1 with two slots,
+  // which fits their registers.
   const int nch = (d + KC - 1) / KC;
-  load_h(hr[0], 0);
-  if (nch > 1) load_h(hr[1], KC);
+  const int nsc = (nch + SC - 1) / SC;
+#pragma unroll
+  for (int t = 0; t < HD; ++t)
+    if (t < nsc) load_h(hr[t], t * KH);
 #pragma unroll
   for (int j = 0; j < PF; ++j)
     if (j < nch) load_w(wr[j], j * KC);
   store_h(hr[0], hs, 0);
+  if (HD < nsc) load_h(hr[0], HD * KH);
   __syncthreads();
-  auto chunk = [&](int c, const bf16x8* cur, bf16x8* pre, bf16x8* h_next, bf16x8* h_free, bool full) {
-    // h_next holds chunk c+1 (loaded two chunks ago); h_free receives c+2.
-    if (full || c + 2 < nch) load_h(h_free, (c + 2) * KC);
+  // jl = c % SC, hb = (c / SC) % 2 and hslot = (c / SC + 1) % HD are static
+  // in the unrolled loops (they start at multiples of U).
+  auto chunk = [&](int c, int jl, int hb, int hslot, const bf16x8* cur, bf16x8* pre, bool full) {
     if (full || c + PF < nch) load_w(pre, (c + PF) * KC);
     __builtin_amdgcn_sched_barrier(0);
-    mma(cur, hs + (c & 1) * BUF);
-    if (full || c + 1 < nch) store_h(h_next, hs + ((c + 1) & 1) * BUF, (c + 1) * KC);
-    __syncthreads();
+    mma(cur, hs + hb * BUF + jl * KC);
+    if (jl == SC - 1) {
+      const int sb = c / SC;
+      if (full || sb + 1 < nsc) store_h(hr[hslot], hs + (hb ^ 1) * BUF, (sb + 1) * KH);
+      __syncthreads();
+      if (full || sb + 1 + HD < nsc) load_h(hr[hslot], (sb + 1 + HD) * KH);
+    }
   };
-  // Steady state: unrolled over lcm(RING, 2) chunks so every register
-  // index is static; all loads in range (c + max(PF, 2) < nch).
-  constexpr int U = RING % 2 == 0 ? RING : 2 * RING;
-  constexpr int AHEAD = PF > 2 ? PF : 2;
+  // Steady state: unrolled over lcm(RING, 2 * SC, HD * SC) chunks so every
+  // register index and buffer offset is static; all loads in range there.
+  constexpr int U = lcm_c(lcm_c(RING, 2 * SC), HD * SC);
+  constexpr int AHEAD = PF + 1 > (HD + 1) * SC ? PF + 1 : (HD + 1) * SC;
   int c = 0;
   for (; c + U - 1 + AHEAD < nch; c += U) {
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      chunk(c + j, wr[j % RING], wr[(j + PF) % RING], hr[(j + 1) & 1], hr[j & 1], true);
+      chunk(c + j, j % SC, (j / SC) & 1, (j / SC + 1) % HD, wr[j % RING], wr[(j + PF) % RING], true);
   }
 #pragma unroll
   for (int j = 0; j < U - 1 + AHEAD; ++j)
     if (c + j < nch)
-      chunk(c + j, wr[j % RING], wr[(j + PF) % RING], hr[(j + 1) & 1], hr[j & 1], false);
+      chunk(c + j, j % SC, (j / SC) & 1, (j / SC + 1) % HD, wr[j % RING], wr[(j + PF) % RING], false);
 
   // Epilogue: lane (r32, h) holds vocab rows v0 + 32q + 8*(r/4) + 4h + r%4
   // (q < RT, r = 0..15) of column n0 + 32f + r32.  Rows are visited in
@@ -348,6 +363,9 @@ constexpr int LM_WAVES = 8;
 // (Dream shape 273 us against 277 us with 256-byte runs, two in flight).
 constexpr int lm_rt(int nf) { return nf <= 3 ? 2 : 1; }
 constexpr int LM_KC = 64;
+// Hidden staging: SC chunks per staged block, HD blocks in flight.
+constexpr int lm_sc(int nf) { return lm_rt(nf) == 2 ? 1 : 2; }
+constexpr int lm_hd(int nf) { return lm_rt(nf) == 2 ? 2 : 1; }
 constexpr int lm_pf(int nf) { return nf == 4 ? 3 : 2; }
 constexpr int lm_vt(int nf) { return 32 * lm_rt(nf) * LM_WAVES; }
 
@@ -418,15 +436,15 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.tiles_total = L.n_vt * L.n_nt;
   p.tiles_per_xcd = (p.tiles_total + 7) / 8;
   const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
-  // The plain kernel assumes d % KC == 0; other d take the RAGGED variant.
-  const bool ragged = d % LM_KC != 0;
+  // The plain kernel assumes d % (KC * SC) == 0; other d take the RAGGED variant.
+  const bool ragged = d % (LM_KC * lm_sc(L.nf)) != 0;
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F)>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_hd(F)>), \
                          grid, block, 0, stream, p);                                          \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F)>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_hd(F)>), \
                          grid, block, 0, stream, p);                                          \
     break;
   switch (L.nf) {
