@@ -103,6 +103,18 @@ def measured_traffic(config):
     return rec.get("hbm_bytes_per_launch")
 
 
+def device_info():
+    """Name, compute-unit count and clock of the GPU the run used (boxes of
+    the same model differ; the per-box context helps read the numbers)."""
+    import torch
+    pr = torch.cuda.get_device_properties(0)
+    info = {"name": pr.name, "cus": pr.multi_processor_count}
+    for key in ("gcnArchName", "clock_rate", "memory_clock_rate"):
+        if hasattr(pr, key):
+            info[key] = getattr(pr, key)
+    return info
+
+
 def cpu_baseline(s):
     """The oracle as it stands, on a bounded sample of the workload: every
     attention head of two query rows per lane, 4 masked rows of the LM head
@@ -415,7 +427,15 @@ def main():
             }
         except Exception as e:   # reported, never silent
             graph = {"error": f"{type(e).__name__}: {e}"}
+        # The box's plain HBM copy rate (torch copy of 1 GiB: 2 GiB moved),
+        # context for the LM-head fraction; boxes of one model differ.
+        src = torch.empty(2**30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        copy_ms = timed(lambda: dst.copy_(src), 5)
+        del src, dst
         return {
+            "hbm_copy_gbs": round(2 * 2**30 / (copy_ms * 1e-3) / 1e9, 1),
             "step_ms_p10_p50_p90": step_p,
             "lmhead_ms_p10_p50_p90": lm_p,
             "attention_cold_ms": round(t_attn_cold, 4),
@@ -444,6 +464,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
+        "device": device_info(),
         "config": {"workload": WORKLOAD_NAMES[args.config], "name": args.config, "seed": args.seed,
                    "L": s.L, "B": s.B, "P": s.P, "Hq": s.Hq, "Hkv": s.Hkv, "D": s.D, "d": s.d,
                    "V": s.V, "N_masked": s.N, "n_refresh": n_ref},

@@ -91,7 +91,7 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 //   steps, and 256*RT vocab rows per workgroup keep the hidden-chunk
 //   traffic at NT/(256*RT) of the W traffic.
 // * Two wavefronts per SIMD: the accumulators take 16*NF*RT registers.
-template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, int HD>
+template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
   constexpr int THREADS = WAVES * 64;
@@ -168,7 +168,7 @@ void lmhead_partial_kernel(LmParams p) {
       for (int r = 0; r < 16; ++r) acc[q][f][r] = 0.f;
 
   constexpr int RING = PF + 1;   // W register slots (chunks)
-  bf16x8 wr[RING][RT * STEPS], hr[HD][HREG];
+  bf16x8 wr[RING][RT * STEPS], hr[HREG];
   auto load_w1 = [&](int q, int kc, int s) {
     const int k = kc + s * 16 + h * 8;
     if (RAGGED) return load_bf16x8(wrow[q] + (k < d ? k : 0));
@@ -212,51 +212,47 @@ void lmhead_partial_kernel(LmParams p) {
 
   // Chunk c (KC columns of K): W in register slot c % RING.  The hidden
   // rows are staged SC chunks at a time: block s (chunks s*SC ..) sits in
-  // LDS buffer s % 2, and a ring of HD register slots holds blocks s + 1
-  // .. s + HD in flight.  At the end of block s, block s + 1 is stored (the
-  // only barrier follows) and its slot is refilled with block s + 1 + HD.
-  // For N > 96, larger blocks (SC = 2, one slot) cost less than one per
-  // chunk (MI355X: Dream 279 -> 270 us, Long 301 -> 292 us, Wide 771 -> 735
-  // us per call); the 64-row kernels (N <= 96) keep SC = 1 with two slots,
-  // which fits their registers.
+  // LDS buffer s % 2 while the registers hr bring block s + 1; at the end
+  // of block s that block is stored (the only barrier follows) and hr is
+  // refilled with block s + 2.  Two-chunk blocks cost less than one
+  // staging step per chunk (MI355X, per call: LLaDA 203 -> 201 us, Dream
+  // 275 -> 269 us, Long 293 -> 286 us, Wide 754 -> 731 us).
   const int nch = (d + KC - 1) / KC;
   const int nsc = (nch + SC - 1) / SC;
-#pragma unroll
-  for (int t = 0; t < HD; ++t)
-    if (t < nsc) load_h(hr[t], t * KH);
+  load_h(hr, 0);
 #pragma unroll
   for (int j = 0; j < PF; ++j)
     if (j < nch) load_w(wr[j], j * KC);
-  store_h(hr[0], hs, 0);
-  if (HD < nsc) load_h(hr[0], HD * KH);
+  store_h(hr, hs, 0);
+  if (nsc > 1) load_h(hr, KH);
   __syncthreads();
-  // jl = c % SC, hb = (c / SC) % 2 and hslot = (c / SC + 1) % HD are static
-  // in the unrolled loops (they start at multiples of U).
-  auto chunk = [&](int c, int jl, int hb, int hslot, const bf16x8* cur, bf16x8* pre, bool full) {
+  // jl = c % SC and hb = (c / SC) % 2 are static in the unrolled loops
+  // (they start at multiples of U).
+  auto chunk = [&](int c, int jl, int hb, const bf16x8* cur, bf16x8* pre, bool full) {
     if (full || c + PF < nch) load_w(pre, (c + PF) * KC);
     __builtin_amdgcn_sched_barrier(0);
     mma(cur, hs + hb * BUF + jl * KC);
     if (jl == SC - 1) {
       const int sb = c / SC;
-      if (full || sb + 1 < nsc) store_h(hr[hslot], hs + (hb ^ 1) * BUF, (sb + 1) * KH);
+      if (full || sb + 1 < nsc) store_h(hr, hs + (hb ^ 1) * BUF, (sb + 1) * KH);
       __syncthreads();
-      if (full || sb + 1 + HD < nsc) load_h(hr[hslot], (sb + 1 + HD) * KH);
+      if (full || sb + 2 < nsc) load_h(hr, (sb + 2) * KH);
     }
   };
-  // Steady state: unrolled over lcm(RING, 2 * SC, HD * SC) chunks so every
-  // register index and buffer offset is static; all loads in range there.
-  constexpr int U = lcm_c(lcm_c(RING, 2 * SC), HD * SC);
-  constexpr int AHEAD = PF + 1 > (HD + 1) * SC ? PF + 1 : (HD + 1) * SC;
+  // Steady state: unrolled over lcm(RING, 2 * SC) chunks so every register
+  // index and buffer offset is static; all loads in range there.
+  constexpr int U = lcm_c(RING, 2 * SC);
+  constexpr int AHEAD = PF + 1 > 2 * SC ? PF + 1 : 2 * SC;
   int c = 0;
   for (; c + U - 1 + AHEAD < nch; c += U) {
 #pragma unroll
     for (int j = 0; j < U; ++j)
-      chunk(c + j, j % SC, (j / SC) & 1, (j / SC + 1) % HD, wr[j % RING], wr[(j + PF) % RING], true);
+      chunk(c + j, j % SC, (j / SC) & 1, wr[j % RING], wr[(j + PF) % RING], true);
   }
 #pragma unroll
   for (int j = 0; j < U - 1 + AHEAD; ++j)
     if (c + j < nch)
-      chunk(c + j, j % SC, (j / SC) & 1, (j / SC + 1) % HD, wr[j % RING], wr[(j + PF) % RING], false);
+      chunk(c + j, j % SC, (j / SC) & 1, wr[j % RING], wr[(j + PF) % RING], false);
 
   // Epilogue: lane (r32, h) holds vocab rows v0 + 32q + 8*(r/4) + 4h + r%4
   // (q < RT, r = 0..15) of column n0 + 32f + r32.  Rows are visited in
@@ -356,17 +352,17 @@ __global__ __launch_bounds__(LM_MERGE_THREADS) void lmhead_merge_kernel(
 
 // ------------------------------------------------------------------ host
 constexpr int LM_WAVES = 8;
-// Row tiles per wavefront, chunk size and chunks in flight per fragment
-// count (no register spills at two wavefronts per SIMD): up to 96 columns
-// two 32-row tiles; above, one tile.  Chunks of 64 K elements (128-byte W
-// runs per row); at 128 columns a third chunk in flight fits and pays
-// (Dream shape 273 us against 277 us with 256-byte runs, two in flight).
+// Row tiles per wavefront and W chunks in flight per fragment count (no
+// register spills at two wavefronts per SIMD): up to 96 columns two 32-row
+// tiles with one chunk in flight (two spill; LLaDA shape 201 us against
+// 205 us); 128 columns one tile and three chunks (Dream shape 273 us
+// against 277 us); above, one tile and two chunks.  Chunks of 64 K
+// elements (128-byte W runs per row), hidden rows staged two chunks at a
+// time.
 constexpr int lm_rt(int nf) { return nf <= 3 ? 2 : 1; }
+constexpr int lm_pf(int nf) { return nf <= 3 ? 1 : (nf == 4 ? 3 : 2); }
 constexpr int LM_KC = 64;
-// Hidden staging: SC chunks per staged block, HD blocks in flight.
-constexpr int lm_sc(int nf) { return lm_rt(nf) == 2 ? 1 : 2; }
-constexpr int lm_hd(int nf) { return lm_rt(nf) == 2 ? 2 : 1; }
-constexpr int lm_pf(int nf) { return nf == 4 ? 3 : 2; }
+constexpr int LM_SC = 2;
 constexpr int lm_vt(int nf) { return 32 * lm_rt(nf) * LM_WAVES; }
 
 // Column tiling: n_nt tiles of nf 32-column fragments (<= 224 columns).
@@ -437,14 +433,14 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.tiles_per_xcd = (p.tiles_total + 7) / 8;
   const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
   // The plain kernel assumes d % (KC * SC) == 0; other d take the RAGGED variant.
-  const bool ragged = d % (LM_KC * lm_sc(L.nf)) != 0;
+  const bool ragged = d % (LM_KC * LM_SC) != 0;
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_hd(F)>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC>), \
                          grid, block, 0, stream, p);                                          \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_hd(F)>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC>), \
                          grid, block, 0, stream, p);                                          \
     break;
   switch (L.nf) {
