@@ -91,7 +91,7 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 //   steps, and 256*RT vocab rows per workgroup keep the hidden-chunk
 //   traffic at NT/(256*RT) of the W traffic.
 // * Two wavefronts per SIMD: the accumulators take 16*NF*RT registers.
-template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC>
+template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, bool ROT>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
   constexpr int THREADS = WAVES * 64;
@@ -217,26 +217,43 @@ void lmhead_partial_kernel(LmParams p) {
   // refilled with block s + 2.  Two-chunk blocks cost less than one
   // staging step per chunk (MI355X, per call: LLaDA 203 -> 201 us, Dream
   // 275 -> 269 us, Long 293 -> 286 us, Wide 754 -> 731 us).
-  const int nch = (d + KC - 1) / KC;
-  const int nsc = (nch + SC - 1) / SC;
-  load_h(hr, 0);
+  //
+  // With ROT the workgroup walks the K blocks in a rotated order (position
+  // sb covers block (sb + rot) % nsc).  Without it, the 512-row workgroups,
+  // which run in step, all read one column offset of W at a time; how those
+  // requests spread over the HBM channels then depends on where W happens
+  // to sit physically.  Six copies of the LLaDA-shape W in one process
+  // took 190-241 us per call unrotated, 186-187 us rotated.  The 256-row
+  // workgroups are not sensitive to it, and lose 2.6% rotated (Dream).
+  // Every position runs all SC chunks of its block, so the chunk count is
+  // nsc * SC (a partial last block's extra chunk reads zeros from the
+  // staged hidden rows).
+  const int nsc = (d + KH - 1) / KH;
+  const int nch = ROT ? nsc * SC : (d + KC - 1) / KC;
+  const int rot = ROT ? (int)(((long long)t * 13) % nsc) : 0;
+  auto kblk = [&](int sb) {
+    const int q = sb + rot;
+    return (q < nsc ? q : q - nsc) * KH;
+  };
+  auto kchunk = [&](int cc) { return kblk(cc / SC) + (cc % SC) * KC; };
+  load_h(hr, kblk(0));
 #pragma unroll
   for (int j = 0; j < PF; ++j)
-    if (j < nch) load_w(wr[j], j * KC);
-  store_h(hr, hs, 0);
-  if (nsc > 1) load_h(hr, KH);
+    if (j < nch) load_w(wr[j], kchunk(j));
+  store_h(hr, hs, kblk(0));
+  if (nsc > 1) load_h(hr, kblk(1));
   __syncthreads();
   // jl = c % SC and hb = (c / SC) % 2 are static in the unrolled loops
   // (they start at multiples of U).
   auto chunk = [&](int c, int jl, int hb, const bf16x8* cur, bf16x8* pre, bool full) {
-    if (full || c + PF < nch) load_w(pre, (c + PF) * KC);
+    if (full || c + PF < nch) load_w(pre, kchunk(c + PF));
     __builtin_amdgcn_sched_barrier(0);
     mma(cur, hs + hb * BUF + jl * KC);
     if (jl == SC - 1) {
       const int sb = c / SC;
-      if (full || sb + 1 < nsc) store_h(hr, hs + (hb ^ 1) * BUF, (sb + 1) * KH);
+      if (full || sb + 1 < nsc) store_h(hr, hs + (hb ^ 1) * BUF, kblk(sb + 1));
       __syncthreads();
-      if (full || sb + 2 < nsc) load_h(hr, (sb + 2) * KH);
+      if (full || sb + 2 < nsc) load_h(hr, kblk(sb + 2));
     }
   };
   // Steady state: unrolled over lcm(RING, 2 * SC) chunks so every register
@@ -437,10 +454,10 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC, lm_rt(F) == 2>), \
                          grid, block, 0, stream, p);                                          \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC, lm_rt(F) == 2>), \
                          grid, block, 0, stream, p);                                          \
     break;
   switch (L.nf) {
