@@ -225,12 +225,15 @@ void lmhead_partial_kernel(LmParams p) {
   // to sit physically.  Six copies of the LLaDA-shape W in one process
   // took 190-241 us per call unrotated, 186-187 us rotated.  The 256-row
   // workgroups are not sensitive to it, and lose 2.6% rotated (Dream).
-  // Every position runs all SC chunks of its block, so the chunk count is
-  // nsc * SC (a partial last block's extra chunk reads zeros from the
-  // staged hidden rows).
+  // Groups of 8 consecutive tiles (one XCD's neighbours) share a rotation,
+  // so a hidden block read by one of them is still in L2 for the others:
+  // per-tile rotations re-fetched it (HBM/MALL fetch 1.125 GB per call
+  // against 1.061 GB, the same time).  Every position runs all SC chunks
+  // of its block, so the chunk count is nsc * SC (a partial last block's
+  // extra chunk reads zeros from the staged hidden rows).
   const int nsc = (d + KH - 1) / KH;
   const int nch = ROT ? nsc * SC : (d + KC - 1) / KC;
-  const int rot = ROT ? (int)(((long long)t * 13) % nsc) : 0;
+  const int rot = ROT ? (int)(((long long)(t >> 3) * 13) % nsc) : 0;
   auto kblk = [&](int sb) {
     const int q = sb + rot;
     return (q < nsc ? q : q - nsc) * KH;
