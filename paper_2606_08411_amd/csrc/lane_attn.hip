@@ -239,19 +239,26 @@ void lane_attn_kernel(AttnParams p) {
     const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
     const f32x16 zero16 = {};
     f32x16 sacc[2];
+    auto kfrag = [&](int kb, int ks) {
+      return *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
+    };
+    if (nsub == 2) {
+      // Both 32-key halves: the two accumulation chains interleave, so
+      // consecutive MFMAs are independent.
+      sacc[0] = zero16;
+      sacc[1] = zero16;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      if (kb < nsub) {
-        sacc[kb] = zero16;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
-          sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
-        }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kb][r] = -INFINITY;
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 a0 = kfrag(0, ks), a1 = kfrag(1, ks);
+        sacc[0] = mfma32x32x16(a0, qf[ks], sacc[0]);
+        sacc[1] = mfma32x32x16(a1, qf[ks], sacc[1]);
       }
+    } else {
+      sacc[0] = zero16;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) sacc[0] = mfma32x32x16(kfrag(0, ks), qf[ks], sacc[0]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[1][r] = -INFINITY;
     }
     if (nvalid < AT_KT) {
 #pragma unroll
