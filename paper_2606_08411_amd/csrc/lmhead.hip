@@ -12,12 +12,13 @@
 // lmhead_partial_kernel is shaped for HBM streaming first and MFMA reuse
 // second (measured on MI355X):
 // * each wavefront owns 32 or 64 vocabulary rows (A operands of the 32x32x16
-//   bf16 MFMA) and loads them straight into registers, two chunks ahead;
-//   each W element is used by one wavefront only;
-// * the chunk of the scored hidden rows (B operand, <= 224 rows per column
-//   tile; more rows take several tiles, each streaming W again) is staged
-//   once per workgroup in LDS and shared by its 8 wavefronts;
+//   bf16 MFMA) and loads them straight into registers, one to three chunks
+//   ahead; each W element is used by one wavefront only;
+// * the scored hidden rows (B operand, <= 224 rows per column tile; more
+//   rows take several tiles, each streaming W again) are staged per block
+//   of K once per workgroup in LDS and shared by its 8 wavefronts;
 // * workgroups are dealt to the 8 XCDs in contiguous runs of vocab tiles;
+//   the 512-row workgroups walk K in a rotated order per group of tiles;
 // * the epilogue writes one partial (m, s, argmax) per column and vocab
 //   tile; lmhead_merge_kernel combines them in a fixed order, so results
 //   are bitwise reproducible.  (A single-kernel merge by the last workgroup
