@@ -113,7 +113,7 @@ def test_lmhead_zero_weight_and_ties():
 
 
 def test_lmhead_repeatable(step_cache):
-    """Repeated calls (sharing the workspace and its arrival counters) give
+    """Repeated calls (sharing the workspace of per-tile partials) give
     bitwise-identical results, also after a call with a different shape."""
     step = step_cache("dream", 0)
     a = _run(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
