@@ -322,7 +322,9 @@ int al_sched_plan(al_sched* s, int32_t* lane_id, uint8_t* role, int32_t* start, 
 /* Blocks of the last plan: tokens [n][W] int32, masked [n][W] uint8. */
 int al_sched_blocks(const al_sched* s, int32_t* tokens, uint8_t* masked);
 /* Results of the last plan: blocks after select_unmask and its lane_stats
- * [n][AL_LANE_STATS].  Returns the number of active lanes afterwards. */
+ * [n][AL_LANE_STATS].  Returns the number of active lanes afterwards, or
+ * AL_ERR_SHAPE (state unchanged) when a lane's split, filled count or
+ * valid length lies outside [0, b_len] or a fork has split 0. */
 int al_sched_commit(al_sched* s, const int32_t* tokens, const uint8_t* masked,
                     const int32_t* lane_stats);
 /* Output reconstruction into out [cap]; returns its length. */

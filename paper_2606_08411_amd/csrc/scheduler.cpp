@@ -137,6 +137,16 @@ int al_sched_commit(al_sched* s, const int32_t* tokens, const uint8_t* masked,
   if (!s) return AL_ERR_NULL;
   const int n = (int)s->plan.size();
   if (n > 0 && (!tokens || !masked || !lane_stats)) return AL_ERR_NULL;
+  // The statistics come from select_unmask on the planned blocks; values
+  // outside a lane's region are rejected before any state changes.
+  for (int i = 0; i < n; ++i) {
+    const int b = s->lanes[s->plan[i]].b;
+    const int32_t* st = lane_stats + (size_t)i * AL_LANE_STATS;
+    if (st[AL_STAT_SPLIT] < 0 || st[AL_STAT_SPLIT] > b || st[AL_STAT_FILLED] < 0 ||
+        st[AL_STAT_FILLED] > b || st[AL_STAT_VALID] < 0 || st[AL_STAT_VALID] > b ||
+        (st[AL_STAT_FORK] && st[AL_STAT_SPLIT] < 1))
+      return AL_ERR_SHAPE;
+  }
   const int W = s->W, L = s->L;
   for (int phase = 0; phase < 2; ++phase) {  // update regions, then window drafts
     for (int i = 0; i < n; ++i) {

@@ -119,3 +119,18 @@ def test_bad_arguments(al):
     S = al.AlSched(0, 16, 8)
     with pytest.raises(al.AsyncLaneError):
         S.plan(cap=0)
+
+
+def test_commit_rejects_bad_statistics(al):
+    """Lane statistics outside the lane's region are rejected and leave the
+    scheduler state as it was."""
+    S = al.AlSched(0, 16, 8)
+    pl = S.plan()
+    tk, mk = S.blocks()
+    good = np.zeros((1, al.LANE_STATS), np.int32)
+    for bad in ([9, 0, 0, 0, 0, 0], [0, -1, 0, 0, 0, 0], [0, 0, 9, 0, 0, 0], [0, 8, 8, 1, 0, 0]):
+        with pytest.raises(al.AsyncLaneError):
+            S.commit(tk, mk, np.array([bad], np.int32))
+        assert S.counters()["iterations"] == 0
+    assert S.commit(tk, mk, good) == 1
+    assert S.counters()["iterations"] == 1
