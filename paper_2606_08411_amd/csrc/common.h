@@ -50,6 +50,19 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const i32x4*>(p));
 }
 
+// LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane j passes the address of the 4 consecutive elements at row j/4,
+// columns 4(j%4)..4(j%4)+3 of a 4 x 16 block of 16-bit elements, and lane i
+// of the group receives column i of that block (rows 0..3 in order).  The
+// four groups' blocks are independent.
+__device__ __forceinline__ bf16x4 lds_read_tr16(const uint16_t* p) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+}
+__device__ __forceinline__ bf16x8 cat_bf16x4(bf16x4 a, bf16x4 b) {
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // s_waitcnt immediate for gfx9-family encodings: wait until at most n vector
 // memory loads are outstanding (n <= 63), no wait on the other counters.
 constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }

@@ -9,20 +9,25 @@
 // Kernel layout.  A workgroup of 4 wavefronts serves one K/V head and four
 // query tiles (32 query rows of one lane and one query head each; for
 // grouped-query attention the Hq/Hkv heads of a lane are adjacent tiles).
-// Key tiles of 64 rows are staged once per workgroup in LDS -- K row-major,
-// V transposed -- and consumed by every wavefront whose lane sees them, so a
-// prefix tile read from HBM serves all lanes of the workgroup.  Both
+// Key tiles of 64 rows are staged once per workgroup in LDS, K and V both
+// row-major as loaded, and consumed by every wavefront whose lane sees them,
+// so a prefix tile read from HBM serves all lanes of the workgroup.  Both
 // products run transposed on the 32x32x16 bf16 MFMA:
 //     S^T = K Q^T      (lane l owns query row l%32, half of the keys)
 //     O^T = V^T P^T    (lane l owns query row l%32, a quarter of D)
 // so the running max / sum of the online softmax and the rescale of O stay
-// inside a lane pair (l, l^32) and need no cross-lane broadcast.  The key
-// order inside each 16-key MFMA step is permuted identically on both
-// operands to match the S^T accumulator layout (a contraction is invariant
-// under a common permutation of its summed index).
+// inside a lane pair (l, l^32) and need no cross-lane broadcast.  The V^T
+// operand comes from LDS transpose reads (ds_read_b64_tr_b16), which hand
+// each lane 4 consecutive keys of one column.  Inside each 16-key MFMA step
+// lane half h takes keys 4h..4h+3 and 8+4h..8+4h+3 on both operands, the
+// keys the S^T accumulator gives it (a contraction is invariant under a
+// common permutation of its summed index).
 //
-// Short grids (few heads x few lanes) split the key tiles over blockIdx.z;
-// the splits' unnormalised partials are combined by attn_merge_kernel.
+// Short grids (few heads x few lanes) either split each query tile's keys
+// over the wavefronts of one workgroup (lane_attn_wsplit_kernel, merged in
+// LDS) or, when that grid would not fit the chip at once, split the key
+// tiles over blockIdx.z, whose unnormalised partials attn_merge_kernel
+// combines.
 #include <math.h>
 
 #include "common.h"
@@ -53,15 +58,6 @@ struct AttnParams {
   unsigned long long vis[AT_MAX_LANES];  // bit j: lane block j visible to lane i
 };
 
-// Position of key kk (within a 64-key tile) in the transposed V tile: inside
-// each 16-key MFMA step, lane half h reads the 8 contiguous positions
-// [8h, 8h+8), which must hold the keys {4h..4h+3, 8+4h..8+4h+3} that the
-// S^T accumulator gives lane half h.
-__device__ __forceinline__ int vt_pos4(int k4) {  // k4 = kk / 4, returns pos of 4*k4
-  const int q = k4 & 3;
-  return 16 * (k4 >> 2) + 8 * (q & 1) + 4 * (q >> 1);
-}
-
 // Two wavefronts per SIMD (<= 256 registers each, no spills at D = 128):
 // with two workgroups per CU, one workgroup's tile staging (loads, the
 // transposed V store, barriers) overlaps the other's MFMAs.  At one
@@ -75,10 +71,10 @@ void lane_attn_kernel(AttnParams p) {
   constexpr int KS = D / 16;       // MFMA k-steps of S^T = K Q^T
   constexpr int DT = D / 32;       // 32-row tiles of O^T
   constexpr int KSTR = D + 8;      // bf16 per K row in LDS (+16 B: spreads banks)
-  constexpr int VSTR = AT_KT + 8;  // bf16 per V^T row in LDS
+  constexpr int VROW = D + 32;     // bf16 per V row in LDS (rows 64 B apart in bank order)
   constexpr int DSEG = D / 8;      // 16-byte segments per K/V row
   __shared__ __attribute__((aligned(16))) uint16_t k_s[AT_KT * KSTR];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_s[D * VSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t v_s[AT_KT * VROW];
 
   const int hk = blockIdx.y;
   const int split = blockIdx.z;
@@ -87,6 +83,8 @@ void lane_attn_kernel(AttnParams p) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar registers and branches
   const int r32 = lane & 31;
   const int hh = lane >> 5;
+  const int lgrp = lane >> 4;  // 16-lane group of the transpose reads
+  const int lg = lane & 15;
   const int per_lane = p.tiles_per_lane * p.g;
 
   // This wavefront's query tile.
@@ -174,12 +172,11 @@ void lane_attn_kernel(AttnParams p) {
     return kt1;
   };
 
-  // Register staging of one tile: K as KREG 16-byte row segments, V as
-  // 4 keys x 8 d blocks (for the transposed LDS copy).
+  // Register staging of one tile: K and V as KREG 16-byte row segments
+  // each; both are stored row-major (V is transposed by the reads).
   constexpr int KREG = (AT_KT * DSEG) / AT_THREADS;
-  constexpr int VPAIRS = (AT_KT / 4) * DSEG;
-  constexpr int VREG = (VPAIRS + AT_THREADS - 1) / AT_THREADS;
-  bf16x8 kr[KREG], vr[VREG][4];
+  static_assert(KREG * AT_THREADS == AT_KT * DSEG, "whole tiles per thread");
+  bf16x8 kr[KREG], vr[KREG];
   auto load_tile = [&](const Tile& tl) {
 #pragma unroll
     for (int i = 0; i < KREG; ++i) {
@@ -189,13 +186,11 @@ void lane_attn_kernel(AttnParams p) {
       kr[i] = load_bf16x8(tl.k + (size_t)min(krow, tl.nvalid - 1) * p.Hkv * D + ds * 8);
     }
 #pragma unroll
-    for (int i = 0; i < VREG; ++i) {
-      const int pr = min(tid + AT_THREADS * i, VPAIRS - 1);
-      const int k4 = pr % (AT_KT / 4);
-      const int ds = pr / (AT_KT / 4);
-#pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4)
-        vr[i][c4] = load_bf16x8(tl.v + (size_t)min(4 * k4 + c4, tl.nvalid - 1) * p.Hkv * D + ds * 8);
+    for (int i = 0; i < KREG; ++i) {
+      const int seg = tid + AT_THREADS * i;
+      const int krow = seg / DSEG;
+      const int ds = seg - krow * DSEG;
+      vr[i] = load_bf16x8(tl.v + (size_t)min(krow, tl.nvalid - 1) * p.Hkv * D + ds * 8);
     }
   };
   // Rows past nvalid are zeroed here (not right after the loads, which
@@ -206,29 +201,9 @@ void lane_attn_kernel(AttnParams p) {
       const int seg = tid + AT_THREADS * i;
       const int krow = seg / DSEG;
       const int ds = seg - krow * DSEG;
-      *reinterpret_cast<bf16x8*>(&k_s[krow * KSTR + ds * 8]) = (nvalid == AT_KT || krow < nvalid) ? kr[i] : zero_bf16x8();
-    }
-#pragma unroll
-    for (int i = 0; i < VREG; ++i) {
-      const int pr = tid + AT_THREADS * i;
-      if (pr >= VPAIRS) break;
-      // Key group fastest across threads: the transposed 8-byte stores of a
-      // wavefront then hit distinct banks (d-segment fastest conflicts 16x).
-      const int k4 = pr % (AT_KT / 4);
-      const int ds = pr / (AT_KT / 4);
-      const int pos = vt_pos4(k4);
-      bf16x8 v4[4];
-#pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) v4[c4] = (nvalid == AT_KT || 4 * k4 + c4 < nvalid) ? vr[i][c4] : zero_bf16x8();
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16x4 col;
-        col[0] = v4[0][e];
-        col[1] = v4[1][e];
-        col[2] = v4[2][e];
-        col[3] = v4[3][e];
-        *reinterpret_cast<bf16x4*>(&vt_s[(ds * 8 + e) * VSTR + pos]) = col;
-      }
+      const bool ok = nvalid == AT_KT || krow < nvalid;
+      *reinterpret_cast<bf16x8*>(&k_s[krow * KSTR + ds * 8]) = ok ? kr[i] : zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&v_s[krow * VROW + ds * 8]) = ok ? vr[i] : zero_bf16x8();
     }
   };
 
@@ -308,13 +283,16 @@ void lane_attn_kernel(AttnParams p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
     }
-    // O^T += V^T P^T, one 16-key MFMA step at a time.
+    // O^T += V^T P^T, one 16-key MFMA step at a time.  The V^T fragment
+    // of lane (d, h) is keys 16 ks2 + 4h + {0..3, 8..11} at column d: two
+    // transpose reads of 4 x 16 blocks of the row-major V tile.
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
       if ((ks2 >> 1) < nsub) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&vt_s[(dt * 32 + r32) * VSTR + ks2 * 16 + hh * 8]);
+          const uint16_t* va = &v_s[(16 * ks2 + 4 * hh + (lg >> 2)) * VROW + dt * 32 + 16 * (lgrp & 1) + 4 * (lg & 3)];
+          const bf16x8 a = cat_bf16x4(lds_read_tr16(va), lds_read_tr16(va + 8 * VROW));
           oacc[dt] = mfma32x32x16(a, pk[ks2], oacc[dt]);
         }
       }
@@ -337,7 +315,7 @@ void lane_attn_kernel(AttnParams p) {
       first.nvalid = 1;
     }
     load_tile(first);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(KREG + 4 * VREG));
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * KREG));
   }
   while (cur.nvalid) {
     __syncthreads();  // the previous tile is no longer read
@@ -386,6 +364,274 @@ void lane_attn_kernel(AttnParams p) {
       pm[0] = m_run;
       pm[1] = l_run;
     }
+  }
+}
+
+// Keys of one query tile split over the wavefronts of one workgroup.
+//
+// On short grids (a few lanes x a few heads) the kernel above leaves most
+// SIMDs idle unless it splits the key range over workgroups, and then its
+// fp32 partials cross a kernel boundary to attn_merge_kernel (written back
+// from L2 at the end of the kernel, read again by the merge).  Here a
+// workgroup of KW wavefronts serves one query tile (32 rows of one lane,
+// one query head).  Wavefront w takes the lane's visible 32-key units w,
+// w + KW, w + 2 KW, ... (prefix units first, then the visible lane blocks
+// in ascending order), stages each in an LDS region of its own and keeps
+// its own online-softmax state; nothing is shared between wavefronts until
+// the end, so the loop has no workgroup barrier.  The KW states are then
+// combined in LDS in ascending w (the same arithmetic as attn_merge_kernel)
+// and the output is written once, in bf16.  Every lane's workgroups re-read
+// the prefix units; workgroup ids run head-fastest, so with Hq a multiple
+// of 8 all query tiles of a head land on one XCD (ids are dealt to the 8
+// XCDs round-robin) and those re-reads hit that XCD's L2.
+template <int D, int KW>
+__global__ __launch_bounds__(KW * kWave) __attribute__((amdgpu_waves_per_eu(KW / 4, KW / 4)))
+void lane_attn_wsplit_kernel(AttnParams p) {
+  constexpr int KT = 32;                    // keys per unit
+  constexpr int KS = D / 16;
+  constexpr int DT = D / 32;
+  constexpr int KSTR = D + 8;
+  constexpr int VROW = D + 32;
+  constexpr int DSEG = D / 8;
+  constexpr int KREG = KT * DSEG / kWave;   // 16-byte K (and V) segments per lane
+  constexpr int WBUF = KT * (KSTR + VROW);  // bf16 per wavefront region
+  constexpr int OSTR = D + 4;               // fp32 per row of the merge area
+  static_assert(KREG * kWave == KT * DSEG, "whole tiles per lane");
+  static_assert((KW * 32 * OSTR + KW * 32 * 2) * 4 <= KW * WBUF * 2, "merge area inside the tile regions");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[KW * WBUF];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r32 = lane & 31;
+  const int hh = lane >> 5;
+  const int lgrp = lane >> 4;
+  const int lg = lane & 15;
+  uint16_t* k_s = lds + w * WBUF;
+  uint16_t* v_s = k_s + KT * KSTR;
+
+  const int hq = blockIdx.x % p.Hq;
+  const int qt = blockIdx.x / p.Hq;
+  const int lane_i = qt / p.tiles_per_lane;
+  const int c = qt - lane_i * p.tiles_per_lane;
+  const int hk = hq / p.g;
+  const int row0 = lane_i * p.rows_per_lane + c * 32;
+  const int nrows = min(min(32, p.rows_per_lane - c * 32), p.n_rows - row0);
+  const unsigned long long vis = p.n_key_lanes ? p.vis[lane_i] : 0ull;
+  const int n_pre = (p.P + KT - 1) / KT;
+  const int lane_units = (p.B_keys + KT - 1) / KT;
+  const int n_units = n_pre + __popcll(vis) * lane_units;
+
+  bf16x8 qf[KS];
+  {
+    const bool ok = r32 < nrows;
+    const uint16_t* qrow = p.q + ((size_t)(row0 + (ok ? r32 : 0)) * p.Hq + hq) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = ok ? load_bf16x8(qrow + ks * 16 + hh * 8) : zero_bf16x8();
+  }
+  f32x16 oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  struct Unit {
+    const uint16_t* k;
+    const uint16_t* v;
+    int nvalid;  // 0 = past the last unit
+  };
+  auto unit_at = [&](int u) -> Unit {
+    Unit t{nullptr, nullptr, 0};
+    if (u >= n_units) return t;
+    int r0;
+    if (u < n_pre) {
+      r0 = u * KT;
+      t.k = p.k_pre + ((size_t)r0 * p.Hkv + hk) * D;
+      t.v = p.v_pre + ((size_t)r0 * p.Hkv + hk) * D;
+      t.nvalid = min(KT, p.P - r0);
+      return t;
+    }
+    const int lu = u - n_pre;
+    int jj = lu / lane_units;
+    const int sub = lu - jj * lane_units;
+    unsigned long long m = vis;
+    for (; jj > 0; --jj) m &= m - 1;  // drop the jj lowest visible lanes
+    r0 = __builtin_ctzll(m) * p.B_keys + sub * KT;
+    t.k = p.k_lane + ((size_t)r0 * p.Hkv + hk) * D;
+    t.v = p.v_lane + ((size_t)r0 * p.Hkv + hk) * D;
+    t.nvalid = min(KT, p.B_keys - sub * KT);
+    return t;
+  };
+
+  bf16x8 kr[KREG], vr[KREG];
+  auto load_unit = [&](const Unit& t) {
+#pragma unroll
+    for (int i = 0; i < KREG; ++i) {
+      const int seg = lane + kWave * i;
+      const int krow = seg / DSEG;
+      const int ds = seg - krow * DSEG;
+      kr[i] = load_bf16x8(t.k + (size_t)min(krow, t.nvalid - 1) * p.Hkv * D + ds * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < KREG; ++i) {
+      const int seg = lane + kWave * i;
+      const int krow = seg / DSEG;
+      const int ds = seg - krow * DSEG;
+      vr[i] = load_bf16x8(t.v + (size_t)min(krow, t.nvalid - 1) * p.Hkv * D + ds * 8);
+    }
+  };
+  auto store_unit = [&](int nvalid) {
+#pragma unroll
+    for (int i = 0; i < KREG; ++i) {
+      const int seg = lane + kWave * i;
+      const int krow = seg / DSEG;
+      const int ds = seg - krow * DSEG;
+      const bool ok = nvalid == KT || krow < nvalid;
+      *reinterpret_cast<bf16x8*>(&k_s[krow * KSTR + ds * 8]) = ok ? kr[i] : zero_bf16x8();
+      *reinterpret_cast<bf16x8*>(&v_s[krow * VROW + ds * 8]) = ok ? vr[i] : zero_bf16x8();
+    }
+  };
+  // S^T = K Q^T in two interleaved chains (even / odd k-steps), the online
+  // softmax update in log2 units, then O^T += V^T P^T -- the arithmetic of
+  // lane_attn_kernel's tile step on one 32-key half.
+  auto unit_compute = [&](int nvalid) {
+    f32x16 s0 = {}, s1 = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ks += 2) {
+      s0 = mfma32x32x16(*reinterpret_cast<const bf16x8*>(&k_s[r32 * KSTR + ks * 16 + hh * 8]), qf[ks], s0);
+      s1 = mfma32x32x16(*reinterpret_cast<const bf16x8*>(&k_s[r32 * KSTR + (ks + 1) * 16 + hh * 8]), qf[ks + 1], s1);
+    }
+    f32x16 s;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = s0[r] + s1[r];
+    if (nvalid < KT) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = 8 * (r >> 2) + 4 * hh + (r & 3);
+        s[r] = (key < nvalid) ? s[r] : -INFINITY;
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
+    mx = pair_max32(mx);
+    const float m_new = fmaxf(m_run, mx * p.scale_log2);
+    const float alpha = exp2_fast(m_run - m_new);
+    float rs = 0.f;
+    bf16x8 pk[2];
+    const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int ks2 = 0; ks2 < 2; ++ks2)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const int r = 8 * ks2 + e;
+        bf16x2 pr;
+        pr[0] = (__bf16)exp2_fast(fmaf(s[r], p.scale_log2, -m_new));
+        pr[1] = (__bf16)exp2_fast(fmaf(s[r + 1], p.scale_log2, -m_new));
+        pk[ks2][e] = pr[0];
+        pk[ks2][e + 1] = pr[1];
+        rs = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, rs, false);
+      }
+    rs = pair_sum32(rs);
+    l_run = l_run * alpha + rs;
+    m_run = m_new;
+    if (__builtin_amdgcn_read_exec() & __ballot(alpha != 1.0f)) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+    }
+#pragma unroll
+    for (int ks2 = 0; ks2 < 2; ++ks2)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint16_t* va = &v_s[(16 * ks2 + 4 * hh + (lg >> 2)) * VROW + dt * 32 + 16 * (lgrp & 1) + 4 * (lg & 3)];
+        const bf16x8 a = cat_bf16x4(lds_read_tr16(va), lds_read_tr16(va + 8 * VROW));
+        oacc[dt] = mfma32x32x16(a, pk[ks2], oacc[dt]);
+      }
+  };
+
+  int u = w;
+  Unit cur = unit_at(u);
+  {
+    // Unconditional first loads and an exact wait for the Q fragments, as
+    // in lane_attn_kernel (a wavefront without a unit reads Q row 0).
+    Unit first = cur;
+    if (!first.nvalid) {
+      first.k = first.v = p.q;
+      first.nvalid = 1;
+    }
+    load_unit(first);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * KREG));
+  }
+  while (cur.nvalid) {
+    // The region is this wavefront's own: its LDS operations complete in
+    // issue order, so wavefront-scope fences (compiler ordering only)
+    // separate the previous unit's reads, this unit's stores and its reads.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    store_unit(cur.nvalid);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    u += KW;
+    const Unit nxt = unit_at(u);
+    if (nxt.nvalid) load_unit(nxt);
+    unit_compute(cur.nvalid);
+    cur = nxt;
+  }
+
+  // Combine the KW states: each wavefront writes (m, l, O) to LDS, then
+  // D / 8 threads per row merge 8 columns each in ascending w.
+  __syncthreads();  // every wavefront is done with its tile region
+  float* o_s = reinterpret_cast<float*>(lds);
+  float* ml_s = o_s + KW * 32 * OSTR;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg)
+      *reinterpret_cast<float4*>(&o_s[(w * 32 + r32) * OSTR + dt * 32 + 8 * rg + 4 * hh]) =
+          make_float4(oacc[dt][rg * 4 + 0], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2], oacc[dt][rg * 4 + 3]);
+  if (hh == 0) {
+    ml_s[(w * 32 + r32) * 2 + 0] = m_run;
+    ml_s[(w * 32 + r32) * 2 + 1] = l_run;
+  }
+  __syncthreads();
+  constexpr int TPR = D / 8;            // threads per row
+  constexpr int RPP = KW * kWave / TPR;  // rows per pass
+  const int d0 = (tid % TPR) * 8;
+  for (int row = tid / TPR; row < nrows; row += RPP) {
+    float mw[KW], M = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < KW; ++ww) {
+      mw[ww] = ml_s[(ww * 32 + row) * 2];
+      M = fmaxf(M, mw[ww]);
+    }
+    float Lsum = 0.f, acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < KW; ++ww) {
+      const float wgt = (mw[ww] == -INFINITY) ? 0.f : exp2_fast(mw[ww] - M);
+      Lsum += ml_s[(ww * 32 + row) * 2 + 1] * wgt;
+      const float4 a = *reinterpret_cast<const float4*>(&o_s[(ww * 32 + row) * OSTR + d0]);
+      const float4 b = *reinterpret_cast<const float4*>(&o_s[(ww * 32 + row) * OSTR + d0 + 4]);
+      acc[0] += a.x * wgt;
+      acc[1] += a.y * wgt;
+      acc[2] += a.z * wgt;
+      acc[3] += a.w * wgt;
+      acc[4] += b.x * wgt;
+      acc[5] += b.y * wgt;
+      acc[6] += b.z * wgt;
+      acc[7] += b.w * wgt;
+    }
+    const float inv = 1.0f / Lsum;
+    bf16x8 out;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = (__bf16)(acc[e] * inv);
+    const size_t orow = (size_t)(row0 + row) * p.Hq + hq;
+    *reinterpret_cast<bf16x8*>(p.o + orow * D + d0) = out;
+    if (p.lse && d0 == 0) p.lse[orow] = (M + log2f(Lsum)) * AT_LN2;
   }
 }
 
@@ -476,18 +722,34 @@ static PassShape pass_shape(int n_rows, int rows_per_lane, int n_lanes, int g, i
   return s;
 }
 
+// The wavefront-split kernel when its grid fits the chip in one round (one
+// workgroup per CU: 256 on MI355X) and no wavefront takes more than 8 key
+// units; otherwise the 4-query-tile kernel, whose shared K/V staging wins
+// on large grids and long key ranges.  Measured per call after a
+// cache-evicting copy (MI355X): LLaDA step shape 16.6 us against 19.7 us,
+// Dream 20.9 against 30.0; Long 56.6 against 57.0 (512 workgroups: stays),
+// Wide 342 against 222, Wide's refresh rows 87 against 67.
+constexpr int kWsplitWaves = 8;
+static bool use_wsplit(const PassShape& s, int Hkv, int max_units) {
+  return s.q_tiles_kv * Hkv <= 256 && max_units <= 8 * kWsplitWaves;
+}
+
 AttnPlan attn_plan(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
   AttnPlan pl{};
   const int g = Hq / Hkv;
+  const int pre_units = (P + 31) / 32;
   const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
-  pl.n_split_lane = L > 0 ? choose_split(a.base_wgs, a.total_key_tiles) : 1;
+  pl.wsplit_lane = L > 0 && use_wsplit(a, Hkv, pre_units + L * ((B + 31) / 32));
+  pl.n_split_lane = (L > 0 && !pl.wsplit_lane) ? choose_split(a.base_wgs, a.total_key_tiles) : 1;
   pl.ws_lane = pl.n_split_lane > 1 ? (size_t)pl.n_split_lane * L * B * Hq * (D + 2) * sizeof(float) : 0;
+  pl.wsplit_ref = false;
   pl.n_split_ref = 1;
   pl.ws_ref = 0;
   if (n_refresh > 0) {
     const int nl = (n_refresh + 31) / 32;
     const PassShape r = pass_shape(n_refresh, 32, nl, g, Hkv, P, 0, 0);
-    pl.n_split_ref = choose_split(r.base_wgs, r.total_key_tiles);
+    pl.wsplit_ref = use_wsplit(r, Hkv, pre_units);
+    pl.n_split_ref = pl.wsplit_ref ? 1 : choose_split(r.base_wgs, r.total_key_tiles);
     pl.ws_ref = pl.n_split_ref > 1 ? (size_t)pl.n_split_ref * n_refresh * Hq * (D + 2) * sizeof(float) : 0;
   }
   pl.total = pl.ws_lane > pl.ws_ref ? pl.ws_lane : pl.ws_ref;
@@ -534,6 +796,21 @@ static hipError_t run_pass(const AttnParams& base, const PassShape& s, int n_spl
   return hipGetLastError();
 }
 
+template <int D, int KW>
+static hipError_t run_pass_wsplit(const AttnParams& base, const PassShape& s, hipStream_t stream) {
+  AttnParams p = base;
+  p.n_rows = s.n_rows;
+  p.rows_per_lane = s.rows_per_lane;
+  p.tiles_per_lane = s.tiles_per_lane;
+  p.q_tiles_kv = s.q_tiles_kv;
+  p.n_pre_tiles = s.n_pre_tiles;
+  p.total_key_tiles = s.total_key_tiles;
+  p.n_split = 1;
+  const unsigned n_wg = (unsigned)(s.q_tiles_kv * p.Hkv);  // one per (query tile, query head)
+  hipLaunchKernelGGL((lane_attn_wsplit_kernel<D, KW>), dim3(n_wg), dim3(KW * kWave), 0, stream, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, const uint16_t* v_lane,
                                  uint16_t* k_pre, uint16_t* v_pre, const unsigned long long* vis,
                                  int L, int B, int P, int Hq, int Hkv, int D, float scale,
@@ -571,8 +848,12 @@ hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, cons
   hipError_t e = hipSuccess;
   if (L > 0) {  // L = 0: refresh-only call
     const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
-    e = (D == 64) ? run_pass<64>(p, a, pl.n_split_lane, ws, stream)
-                  : run_pass<128>(p, a, pl.n_split_lane, ws, stream);
+    if (pl.wsplit_lane)
+      e = (D == 64) ? run_pass_wsplit<64, kWsplitWaves>(p, a, stream)
+                    : run_pass_wsplit<128, kWsplitWaves>(p, a, stream);
+    else
+      e = (D == 64) ? run_pass<64>(p, a, pl.n_split_lane, ws, stream)
+                    : run_pass<128>(p, a, pl.n_split_lane, ws, stream);
   }
   if (e != hipSuccess || n_refresh <= 0) return e;
 
@@ -589,6 +870,9 @@ hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, cons
   for (int i = 0; i < AT_MAX_LANES; ++i) r.vis[i] = 0ull;
   const int nl = (n_refresh + 31) / 32;
   const PassShape b = pass_shape(n_refresh, 32, nl, g, Hkv, P, 0, 0);
+  if (pl.wsplit_ref)
+    return (D == 64) ? run_pass_wsplit<64, kWsplitWaves>(r, b, stream)
+                     : run_pass_wsplit<128, kWsplitWaves>(r, b, stream);
   return (D == 64) ? run_pass<64>(r, b, pl.n_split_ref, ws, stream)
                    : run_pass<128>(r, b, pl.n_split_ref, ws, stream);
 }

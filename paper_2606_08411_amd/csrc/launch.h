@@ -8,7 +8,8 @@ namespace al {
 
 // ---- lane attention
 struct AttnPlan {
-  int n_split_lane, n_split_ref;
+  bool wsplit_lane, wsplit_ref;  // keys split over the wavefronts of a workgroup
+  int n_split_lane, n_split_ref;  // else: key splits over workgroups
   size_t ws_lane, ws_ref, total;
 };
 AttnPlan attn_plan(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh);

@@ -95,9 +95,16 @@ SWEEP = [
     (64, 16, 12, "forest", 16, 2, 257, 0.3),
     (128, 32, 6, "linear", 28, 4, 130, 0.1),
     (64, 1024, 2, "fork", 16, 1, 64, 0.0),      # largest block, largest GQA group
-    (128, 32, 64, "forest", 4, 1, 0, 0.0),      # no prefix, 64 roots: many key splits
-                                                # hold no tile any wavefront of a
+    (128, 32, 64, "forest", 4, 1, 0, 0.0),      # no prefix, 64 roots: 256 workgroups of
+                                                # the wavefront-split kernel, 64 units
+    (128, 32, 64, "forest", 8, 2, 0, 0.0),      # the same on the 4-tile kernel: many key
+                                                # splits hold no tile any wavefront of a
                                                 # workgroup sees (empty-split path)
+    (128, 48, 12, "random", 16, 2, 333, 0.2),   # 4-tile kernel (384 query tiles) with
+                                                # 2 row tiles per lane; refresh rows on
+                                                # the wavefront-split kernel
+    (128, 16, 40, "random", 4, 2, 700, 0.0),    # wavefront-split kernel at its unit
+                                                # limit (62 units), ragged prefix
 ]
 
 
