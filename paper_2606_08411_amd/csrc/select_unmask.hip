@@ -70,6 +70,11 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   __shared__ int s_arg[kSelMaxPositions];
   __shared__ int s_lo[kSelMaxLanes], s_hi[kSelMaxLanes], s_cnt[kSelMaxLanes], s_nsel[kSelMaxLanes];
   __shared__ int s_blen[kSelMaxLanes], s_k[kSelMaxLanes], s_role[kSelMaxLanes], s_ndraft[kSelMaxLanes];
+  __shared__ int s_tlane[kSelMaxLanes];
+  // Delimiter, digit, open- and close-bracket ids.
+  constexpr int ID_DIGIT = kSelMaxDelims, ID_OPEN = ID_DIGIT + kSelMaxBoundaryIds;
+  constexpr int ID_CLOSE = ID_OPEN + kSelMaxBoundaryIds, ID_ALL = ID_CLOSE + kSelMaxBoundaryIds;
+  __shared__ int32_t s_ids[ID_ALL];
   __shared__ int s_wu[SEL_WAVES], s_ws[SEL_WAVES];
 
   const SelHost& h = p.h;
@@ -95,8 +100,16 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     s_blen[tid] = tid < L ? h.b_len[tid] : 0;
     s_k[tid] = tid < L ? h.k_lane[tid] : 0;
     s_role[tid] = tid < L ? h.role[tid] : 1;
+    s_tlane[tid] = tid < L ? h.t_lane[tid] : 0;
     s_ndraft[tid] = 0;
   }
+  // The per-lane limits and id sets live in the kernel arguments; copied
+  // here in one parallel step, the later phases read them from LDS instead
+  // of issuing dependent scalar loads.
+  if (tid < ID_DIGIT) s_ids[tid] = h.delim[tid];
+  else if (tid < ID_OPEN) s_ids[tid] = h.digit[tid - ID_DIGIT];
+  else if (tid < ID_CLOSE) s_ids[tid] = h.open[tid - ID_OPEN];
+  else if (tid < ID_ALL) s_ids[tid] = h.close[tid - ID_CLOSE];
   __syncthreads();
 
   // Candidates, lane row ranges (row_pos is ascending, so each lane's rows
@@ -118,24 +131,28 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
         s_arg[n] != h.eos_id)
       f |= SEL_DRAFT;
     s_sel[n] = f;
+    if (!cand) s_conf[n] = __builtin_nanf("");  // compares false in the ranking below
   }
   __syncthreads();
 
   // Top-k (TOPK mode) or fallback (THRESHOLD mode, lanes with no pass):
-  // a candidate is chosen when fewer than k candidates of its lane beat it.
+  // a candidate is chosen when fewer than k candidates of its lane come
+  // first (higher confidence, or equal confidence and lower position).
+  // row_pos is strictly ascending, so on equal confidence exactly the
+  // lane's earlier rows come first; non-candidates hold NaN, which compares
+  // false.  One LDS read per compared row, no branch.
   for (int n = tid; n < N; n += SEL_THREADS) {
     if (!(s_sel[n] & SEL_CANDIDATE)) continue;
-    const int pos = s_pos[n];
-    const int ln = pos / B;
+    const int ln = s_pos[n] / B;
     const int k = (h.mode == 1) ? s_k[ln] : (s_cnt[ln] == 0 ? h.fallback_k : 0);
     if (k <= 0) continue;
     const float c = s_conf[n];
+    const int lo = s_lo[ln], hi = s_hi[ln];
     int rank = 0;
-    for (int m = s_lo[ln]; m < s_hi[ln]; ++m) {
-      if (!(s_sel[m] & SEL_CANDIDATE)) continue;
-      const float cm = s_conf[m];
-      rank += (cm > c) || (cm == c && s_pos[m] < pos);
-    }
+#pragma unroll 8
+    for (int m = lo; m < n; ++m) rank += s_conf[m] >= c;
+#pragma unroll 8
+    for (int m = n + 1; m < hi; ++m) rank += s_conf[m] > c;
     if (rank < k) s_sel[n] |= SEL_TRANSFER;
   }
   __syncthreads();
@@ -202,7 +219,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     return hit;
   };
   for (int ln = w; ln < L; ln += SEL_WAVES) {
-    const int n = h.b_len[ln];
+    const int n = s_blen[ln];
     int last = -1, filled = 0, stop = n, carry = 0;
     for (int i0 = 0; i0 < B; i0 += kWave) {
       const int i = i0 + lane;
@@ -211,7 +228,7 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
       const bool m = in ? s_msk[pos] != 0 : true;
       const int tk = in ? s_tok[pos] : 0;
       int delta = 0;
-      if (in && !m) delta = in_set(tk, h.open, h.n_open) ? 1 : (in_set(tk, h.close, h.n_close) ? -1 : 0);
+      if (in && !m) delta = in_set(tk, s_ids + ID_OPEN, h.n_open) ? 1 : (in_set(tk, s_ids + ID_CLOSE, h.n_close) ? -1 : 0);
       int depth = delta;
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) {
@@ -224,8 +241,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
       if (in) {
         if (!m) {
           ++filled;
-          isd = in_set(tk, h.delim, h.n_delim) && depth <= 0;
-          if (isd && i > 0 && !s_msk[pos - 1] && in_set(s_tok[pos - 1], h.digit, h.n_digit)) isd = false;
+          isd = in_set(tk, s_ids, h.n_delim) && depth <= 0;
+          if (isd && i > 0 && !s_msk[pos - 1] && in_set(s_tok[pos - 1], s_ids + ID_DIGIT, h.n_digit)) isd = false;
         }
         if (isd) last = i;
         if (m || tk == h.eos_id) stop = min(stop, i);
@@ -237,8 +254,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
     stop = wave_min(stop);
     if (lane == 0) {
       const int split = last + 1;
-      const bool fork = h.role[ln] == 0 && split > 0 &&
-                        (float)filled >= h.rho_min * (float)n && h.t_lane[ln] >= h.t_min;
+      const bool fork = s_role[ln] == 0 && split > 0 &&
+                        (float)filled >= h.rho_min * (float)n && s_tlane[ln] >= h.t_min;
       int32_t* st = p.lane_stats + ln * 6;
       st[0] = split;
       st[1] = filled;
