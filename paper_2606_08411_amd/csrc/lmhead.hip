@@ -83,11 +83,11 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 //   ahead (lane half h of row r takes K elements kc + 16s + 8h .. +8; over
 //   a chunk each row is read as one 2*KC-byte run).  Each W element is used
 //   by one wavefront only.
-// * The hidden chunk (NT x KC) is double-buffered in LDS, one barrier per
-//   chunk, and shared by the workgroup's wavefronts.  Its loads go into a
-//   two-deep register ring issued two chunks ahead and before the W
-//   prefetch, so the wait for them (the load counter is in-order) never
-//   waits for W loads that are still needed later.
+// * The hidden rows are staged in blocks of SC chunks (NT x KC*SC),
+//   double-buffered in LDS with one barrier per block and shared by the
+//   workgroup's wavefronts.  The next block's loads go into registers one
+//   block ahead, issued before the W prefetch, so the wait for them (the
+//   load counter is in order) never waits for W loads still needed later.
 // * 32-row A tiles halve the B-operand LDS reads per FLOP of 16x16x32
 //   steps, and 256*RT vocab rows per workgroup keep the hidden-chunk
 //   traffic at NT/(256*RT) of the W traffic.
@@ -378,12 +378,16 @@ constexpr int LM_WAVES = 8;
 // tiles with one chunk in flight (two spill; LLaDA shape 201 us against
 // 205 us); 128 columns one tile and three chunks (Dream shape 273 us
 // against 277 us); above, one tile and two chunks.  Chunks of 64 K
-// elements (128-byte W runs per row), hidden rows staged two chunks at a
-// time.
+// elements (128-byte W runs per row).  Hidden rows are staged four chunks
+// at a time up to 96 columns (LLaDA shape over six W placements: 186.5 us
+// against 187.8 us with two; 101 KB of LDS, 243 registers), two above.
+// Rejected for up to 96 columns: 32-element chunks three or four ahead
+// (207 / 199.5 us: shorter runs per row), one 32-row tile with
+// 128-element chunks one or two ahead (196-210 us).
 constexpr int lm_rt(int nf) { return nf <= 3 ? 2 : 1; }
 constexpr int lm_pf(int nf) { return nf <= 3 ? 1 : (nf == 4 ? 3 : 2); }
+constexpr int lm_sc(int nf) { return nf <= 3 ? 4 : 2; }
 constexpr int LM_KC = 64;
-constexpr int LM_SC = 2;
 constexpr int lm_vt(int nf) { return 32 * lm_rt(nf) * LM_WAVES; }
 
 // Column tiling: n_nt tiles of nf 32-column fragments (<= 224 columns).
@@ -454,14 +458,13 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.tiles_per_xcd = (p.tiles_total + 7) / 8;
   const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
   // The plain kernel assumes d % (KC * SC) == 0; other d take the RAGGED variant.
-  const bool ragged = d % (LM_KC * LM_SC) != 0;
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
-    if (ragged)                                                                               \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC, lm_rt(F) == 2>), \
+    if (d % (LM_KC * lm_sc(F)) != 0)                                                          \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_rt(F) == 2>), \
                          grid, block, 0, stream, p);                                          \
     else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), LM_SC, lm_rt(F) == 2>), \
+      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_rt(F) == 2>), \
                          grid, block, 0, stream, p);                                          \
     break;
   switch (L.nf) {
