@@ -191,9 +191,10 @@ def decode_bench(args):
     q, kl, vl = pool(64 * Wb, s.Hq), pool(64 * Wb, s.Hkv), pool(64 * Wb, s.Hkv)
     kp, vp = pool(s.P + L, s.Hkv), pool(s.P + L, s.Hkv)
 
-    # Host <-> device traffic per iteration goes through pinned staging
-    # buffers: one upload (row ids, rows, suppress flags, tokens, masks) and
-    # three asynchronous downloads waited for once.  Separate synchronous
+    # Host <-> device traffic per iteration goes through one pinned staging
+    # buffer: one upload (row ids, rows, suppress flags, tokens, masks) and
+    # one download (tokens, masks and lane statistics, adjacent sections the
+    # selection updates in place), waited for once.  Separate synchronous
     # copies from pageable memory cost ~140 us per iteration.
     cap = 64 * Wb
     sec = [0]
@@ -201,14 +202,22 @@ def decode_bench(args):
         off = sec[0]
         sec[0] += -(-nbytes // 256) * 256
         return off
-    o_ridx, o_rows, o_tok = section(4 * cap), section(4 * cap), section(4 * cap)
-    o_sup, o_msk = section(cap), section(cap)
+    o_ridx, o_rows, o_sup = section(4 * cap), section(4 * cap), section(cap)
+    o_tok, o_msk, o_st = section(4 * cap), section(cap), section(4 * 64 * al.LANE_STATS)
     up_h = torch.empty(sec[0], dtype=torch.uint8, pin_memory=True)
     up_d = torch.empty(sec[0], dtype=torch.uint8, device=dev)
     up_np = up_h.numpy()
-    tok_h = torch.empty(cap, dtype=torch.int32, pin_memory=True)
-    msk_h = torch.empty(cap, dtype=torch.uint8, pin_memory=True)
-    st_h = torch.empty((64, al.LANE_STATS), dtype=torch.int32, pin_memory=True)
+    down_h = torch.empty(sec[0] - o_tok, dtype=torch.uint8, pin_memory=True)
+    down_np = down_h.numpy()
+    # Device outputs allocated once (capacity-sized; each call uses a prefix).
+    conf_d = torch.empty(cap, dtype=torch.float32, device=dev)
+    arg_d = torch.empty(cap, dtype=torch.int32, device=dev)
+    sel_out = dict(unmask_flag=torch.empty(cap, dtype=torch.uint8, device=dev),
+                   unmasked_pos=torch.empty(cap, dtype=torch.int32, device=dev),
+                   still_masked_pos=torch.empty(cap, dtype=torch.int32, device=dev),
+                   counts=torch.empty(2, dtype=torch.int32, device=dev),
+                   lane_stats=up_d[o_st:].view(torch.int32).view(64, al.LANE_STATS),
+                   delim_flag=None)
 
     def one_decode():
         S = al.AlSched(s.P, L, B, window, 64)
@@ -236,23 +245,23 @@ def decode_bench(args):
             up_np[o_tok:o_tok + 4 * nb].view(np.int32)[:] = tk
             up_np[o_sup:o_sup + nr] = pl["role"][rows // Wb] == al.ROLE_REF
             up_np[o_msk:o_msk + nb] = mk
-            up_d[:sec[0]].copy_(up_h, non_blocking=True)
+            up_d[:o_st].copy_(up_h[:o_st], non_blocking=True)
             row_idx = up_d[o_ridx:o_ridx + 4 * nr].view(torch.int32)
             rows_d = up_d[o_rows:o_rows + 4 * nr].view(torch.int32)
             tok_d = up_d[o_tok:o_tok + 4 * nb].view(torch.int32)
             sup = up_d[o_sup:o_sup + nr]
             msk_d = up_d[o_msk:o_msk + nb]
             conf, arg, _ = al.lmhead_confidence(H, W, row_idx=row_idx, suppress_eos=sup,
-                                                eos_id=s.eos_id, want_lse=False)
-            out = al.select_unmask(conf, arg, rows_d, tok_d, msk_d, n, Wb,
-                                   pl["role"], pl["b_len"], pl["t_step"], al.MODE_THRESHOLD, s.tau,
-                                   1, None, s.delim_ids, s.eos_id, s.rho_min, s.t_min,
-                                   tau_future=s.tau, with_delim_flag=False)
-            tok_h[:nb].copy_(tok_d, non_blocking=True)
-            msk_h[:nb].copy_(msk_d, non_blocking=True)
-            st_h[:n].copy_(out["lane_stats"], non_blocking=True)
+                                                eos_id=s.eos_id, conf=conf_d, argmax=arg_d,
+                                                want_lse=False)
+            al.select_unmask(conf, arg, rows_d, tok_d, msk_d, n, Wb,
+                             pl["role"], pl["b_len"], pl["t_step"], al.MODE_THRESHOLD, s.tau,
+                             1, None, s.delim_ids, s.eos_id, s.rho_min, s.t_min,
+                             tau_future=s.tau, with_delim_flag=False, out=sel_out)
+            down_h.copy_(up_d[o_tok:], non_blocking=True)
             torch.cuda.current_stream().synchronize()
-            S.commit(tok_h[:nb].numpy(), msk_h[:nb].numpy(), st_h[:n].numpy())
+            S.commit(down_np[:4 * nb].view(np.int32), down_np[o_msk - o_tok:o_msk - o_tok + nb],
+                     down_np[o_st - o_tok:o_st - o_tok + 4 * n * al.LANE_STATS].view(np.int32))
         return S, attn_calls
 
     one_decode()   # warm-up

@@ -93,11 +93,20 @@ def _ptr(t):
         raise AsyncLaneError("device tensor expected")
     if not t.is_contiguous():
         raise AsyncLaneError("contiguous tensor expected")
-    return ctypes.c_void_p(t.data_ptr())
+    return t.data_ptr()
 
 
-def _stream():
-    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+# torch's raw-handle accessor costs ~0.1 us against ~3 us for
+# torch.cuda.current_stream(); both name the same stream.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream(t=None):
+    """Handle of torch's current stream on t's device (else the current device)."""
+    idx = t.device.index if t is not None else torch.cuda.current_device()
+    if _raw_stream is not None:
+        return _raw_stream(idx)
+    return torch.cuda.current_stream(idx).cuda_stream
 
 
 def _host_i32(x, n, name):
@@ -115,7 +124,21 @@ def _host_u8(x, n, name):
 
 
 def _np_ptr(a):
-    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+    return None if a is None else a.ctypes.data
+
+
+_id_sets: dict = {}
+
+
+def _host_ids(x):
+    """int32 array of a token-id set; tuples and lists are converted once."""
+    if isinstance(x, (tuple, list)):
+        key = tuple(int(v) for v in x)
+        a = _id_sets.get(key)
+        if a is None:
+            a = _id_sets[key] = np.asarray(key, dtype=np.int32)
+        return a
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
 
 
 # ------------------------------------------------------------ workspaces
@@ -184,7 +207,8 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
         _ptr(refresh_idx) if n_ref else None, n_ref,
         _ptr(q_ref) if n_ref else None, _ptr(k_ref) if n_ref else None,
         _ptr(v_ref) if n_ref else None, _ptr(o_ref) if n_ref else None,
-        _ptr(lse_ref) if n_ref else None, _ptr(o), _ptr(lse), _ptr(ws), ws_bytes, _stream())
+        _ptr(lse_ref) if n_ref else None, _ptr(o), _ptr(lse), _ptr(ws), ws_bytes,
+        _stream(k_prefix))
     _check(st, "lane_attn_forward")
     return o, lse, o_ref, lse_ref
 
@@ -231,7 +255,7 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
         ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
     st = lib.lmhead_confidence(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
                                _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
-                               _ptr(lse), _ptr(ws), ws_bytes, _stream())
+                               _ptr(lse), _ptr(ws), ws_bytes, _stream(hidden))
     _check(st, "lmhead_confidence")
     return conf, argmax, lse
 
@@ -253,8 +277,8 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
     b_len_h = None if b_len is None else _host_i32(b_len, L, "b_len")
     t_lane_h = None if t_lane is None else _host_i32(t_lane, L, "t_lane")
     k_lane_h = None if k_lane is None else _host_i32(k_lane, L, "k_lane")
-    delim_h = np.ascontiguousarray(np.asarray(delim_ids, dtype=np.int32))
-    sets = [np.ascontiguousarray(np.asarray(x, dtype=np.int32)) for x in (digit_ids, open_ids, close_ids)]
+    delim_h = _host_ids(delim_ids)
+    sets = [_host_ids(x) for x in (digit_ids, open_ids, close_ids)]
     if out is None:
         out = dict(
             unmask_flag=torch.empty(max(N, 1), dtype=torch.uint8, device=dev),
@@ -274,7 +298,7 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
         int(t_min), float("inf") if tau_future is None else float(tau_future),
         _ptr(out["unmask_flag"]), _ptr(out["unmasked_pos"]),
         _ptr(out["still_masked_pos"]), _ptr(out["counts"]), _ptr(out["lane_stats"]),
-        _ptr(out["delim_flag"]), _stream())
+        _ptr(out["delim_flag"]), _stream(tokens))
     _check(st, "select_unmask")
     return out
 
@@ -292,34 +316,41 @@ class AlSched:
         if not self._h:
             raise AsyncLaneError("al_sched_create: bad arguments")
         self._n = 0
+        # Output buffers reused across calls, with their addresses cached
+        # (numpy's pointer lookup costs ~1 us per array).
+        self._plan_bufs = {}
+        nb = max(int(max_lanes), 1) * self.W
+        self._blk = (np.zeros(nb, np.int32), np.zeros(nb, np.uint8))
+        self._blk_ptr = tuple(x.ctypes.data for x in self._blk)
 
     def __del__(self):
         if getattr(self, "_h", None):
             self._lib.al_sched_destroy(self._h)
             self._h = None
 
+    _PLAN_KEYS = ("lane_id", "role", "start", "b_len", "t_step", "group", "call_parent")
+
     def plan(self, cap=64):
         """Returns dict of [n] arrays: lane_id, role, start, b_len, t_step,
         group, call_parent."""
-        a = dict(lane_id=np.zeros(cap, np.int32), role=np.zeros(cap, np.uint8),
-                 start=np.zeros(cap, np.int32), b_len=np.zeros(cap, np.int32),
-                 t_step=np.zeros(cap, np.int32), group=np.zeros(cap, np.int32),
-                 call_parent=np.zeros(cap, np.int32))
-        n = self._lib.al_sched_plan(self._h, *[_np_ptr(a[k]) for k in
-                                              ("lane_id", "role", "start", "b_len", "t_step",
-                                               "group", "call_parent")], cap)
+        bufs = self._plan_bufs.get(cap)
+        if bufs is None:
+            arrs = [np.zeros(cap, np.uint8 if k == "role" else np.int32) for k in self._PLAN_KEYS]
+            bufs = self._plan_bufs[cap] = (arrs, [x.ctypes.data for x in arrs])
+        arrs, ptrs = bufs
+        n = self._lib.al_sched_plan(self._h, *ptrs, cap)
         if n < 0:
             _check(n, "al_sched_plan")
         self._n = n
-        return {k: v[:n].copy() for k, v in a.items()}
+        return {k: x[:n].copy() for k, x in zip(self._PLAN_KEYS, arrs)}
 
     def blocks(self):
-        tk = np.zeros(max(self._n, 1) * self.W, np.int32)
-        mk = np.zeros(max(self._n, 1) * self.W, np.uint8)
-        r = self._lib.al_sched_blocks(self._h, _np_ptr(tk), _np_ptr(mk))
+        """Tokens and mask flags of the planned lanes' blocks, [n * (B + window)]."""
+        r = self._lib.al_sched_blocks(self._h, *self._blk_ptr)
         if r < 0:
             _check(r, "al_sched_blocks")
-        return tk[:self._n * self.W], mk[:self._n * self.W]
+        m = self._n * self.W
+        return self._blk[0][:m].copy(), self._blk[1][:m].copy()
 
     def commit(self, tokens, masked, lane_stats):
         tk = np.ascontiguousarray(tokens, np.int32)
