@@ -379,14 +379,15 @@ constexpr int LM_WAVES = 8;
 // 205 us); 128 columns one tile and three chunks (Dream shape 273 us
 // against 277 us); above, one tile and two chunks.  Chunks of 64 K
 // elements (128-byte W runs per row).  Hidden rows are staged four chunks
-// at a time up to 96 columns (LLaDA shape over six W placements: 186.5 us
-// against 187.8 us with two; 101 KB of LDS, 243 registers), two above.
+// at a time up to 128 columns (over six W placements: LLaDA shape 186.5 us
+// against 187.8 us with two, 101 KB of LDS, 243 registers; Dream shape
+// 260.3 us against 264.4 us, 135 KB, 224 registers), two above.
 // Rejected for up to 96 columns: 32-element chunks three or four ahead
 // (207 / 199.5 us: shorter runs per row), one 32-row tile with
 // 128-element chunks one or two ahead (196-210 us).
 constexpr int lm_rt(int nf) { return nf <= 3 ? 2 : 1; }
 constexpr int lm_pf(int nf) { return nf <= 3 ? 1 : (nf == 4 ? 3 : 2); }
-constexpr int lm_sc(int nf) { return nf <= 3 ? 4 : 2; }
+constexpr int lm_sc(int nf) { return nf <= 4 ? 4 : 2; }
 constexpr int LM_KC = 64;
 constexpr int lm_vt(int nf) { return 32 * lm_rt(nf) * LM_WAVES; }
 
