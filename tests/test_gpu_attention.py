@@ -117,6 +117,36 @@ def test_attention_sweep(case):
     _check_full(step, out)
 
 
+def _random_cases(n=10, seed=2606):
+    """Seeded random valid shapes on both sides of the kernel choice (at
+    most 256 query tiles x heads and 64 32-key units per tile take the
+    wavefront-split kernel, larger ones the 4-tile kernel)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for k in range(n):
+        big = k % 2 == 1          # long prefix or many heads: the 4-tile kernel
+        Hkv = int(rng.choice([4, 8] if big else [1, 2, 4]))
+        g = int(rng.choice([2, 4] if big else [1, 2, 4, 7]))
+        L = int(rng.integers(6, 11) if big else rng.integers(1, 13))
+        P = int(rng.integers(1000, 2200) if big else rng.integers(0, 700))
+        cases.append((int(rng.choice([64, 128])), int(rng.choice([32, 48] if big else [16, 32, 48, 64])),
+                      L, str(rng.choice(["linear", "fork", "random", "forest"])),
+                      Hkv * g, Hkv, P, float(rng.choice([0.0, 0.0, 0.1]))))
+    return cases
+
+
+RANDOM = _random_cases(12)
+
+
+@pytest.mark.parametrize("case", RANDOM, ids=[str(c) for c in RANDOM])
+def test_attention_random_shapes(case):
+    D, B, L, tree, Hq, Hkv, P, rf = case
+    step = synth.make_step("tiny", 9, with_weight=False, D=D, B=B, L=L, tree=tree, Hq=Hq, Hkv=Hkv,
+                           P=P, refresh_frac=rf, depth_max=4, V=64, d=64)
+    out = _run(step)
+    _check_full(step, out)
+
+
 def test_attention_closed_forms():
     """V = 1 gives O = 1 exactly; K = 0 gives the mean of the visible V rows."""
     step = synth.make_step("tiny", 11, with_weight=False, L=5, tree="random", depth_max=3, P=70, B=32)
