@@ -15,8 +15,8 @@
 // reads every input once into LDS (one memory latency instead of one per
 // phase or per loop iteration), ranks top-k candidates by comparison
 // counting (ties: lower position first), compacts the unmasked /
-// still-masked row lists in order with wavefront ballots, and reduces each
-// lane's statistics with wavefront shuffles.
+// still-masked row lists in order with wavefront ballots, and reads each
+// lane's statistics off wavefront ballots.
 #include "common.h"
 #include "launch.h"
 
@@ -44,22 +44,6 @@ struct SelParams {
 constexpr uint8_t SEL_TRANSFER = 1;   // chosen by the transfer rule
 constexpr uint8_t SEL_CANDIDATE = 2;  // masked, inside [0, b_len)
 constexpr uint8_t SEL_DRAFT = 4;      // lookahead draft
-
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
-__device__ __forceinline__ int wave_max(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, kWave));
-  return v;
-}
-__device__ __forceinline__ int wave_min(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o, kWave));
-  return v;
-}
 
 __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p) {
   __shared__ int s_tok[kSelMaxPositions];
@@ -210,14 +194,18 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   }
 
   // Lane boundary statistics on the updated state: one wavefront per lane,
-  // 64 positions per pass.  ValidBoundary: the bracket depth of [0, i] is
-  // an inclusive wavefront prefix sum plus the depth carried from earlier
-  // passes; the numeric-period test reads position i-1.
+  // 64 positions per pass.  The last delimiter, the filled count and the
+  // first masked / EOS position come from wavefront ballots (uniform
+  // results, no shuffle reductions).  ValidBoundary: the bracket depth of
+  // [0, i] is an inclusive wavefront prefix sum plus the depth carried
+  // from earlier passes (only when bracket ids are given); the
+  // numeric-period test reads position i-1.
   auto in_set = [](int tk, const int32_t* set, int n) {
     bool hit = false;
     for (int j = 0; j < n; ++j) hit |= (tk == set[j]);
     return hit;
   };
+  const bool brackets = (h.n_open | h.n_close) != 0;
   for (int ln = w; ln < L; ln += SEL_WAVES) {
     const int n = s_blen[ln];
     int last = -1, filled = 0, stop = n, carry = 0;
@@ -227,31 +215,30 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
       const bool in = i < n;
       const bool m = in ? s_msk[pos] != 0 : true;
       const int tk = in ? s_tok[pos] : 0;
-      int delta = 0;
-      if (in && !m) delta = in_set(tk, s_ids + ID_OPEN, h.n_open) ? 1 : (in_set(tk, s_ids + ID_CLOSE, h.n_close) ? -1 : 0);
-      int depth = delta;
+      int depth = 0;
+      if (brackets) {
+        if (in && !m) depth = in_set(tk, s_ids + ID_OPEN, h.n_open) ? 1 : (in_set(tk, s_ids + ID_CLOSE, h.n_close) ? -1 : 0);
 #pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int v = __shfl_up(depth, o, kWave);
-        if (lane >= o) depth += v;
-      }
-      depth += carry;
-      carry = __shfl(depth, kWave - 1, kWave);
-      bool isd = false;
-      if (in) {
-        if (!m) {
-          ++filled;
-          isd = in_set(tk, s_ids, h.n_delim) && depth <= 0;
-          if (isd && i > 0 && !s_msk[pos - 1] && in_set(s_tok[pos - 1], s_ids + ID_DIGIT, h.n_digit)) isd = false;
+        for (int o = 1; o < kWave; o <<= 1) {
+          const int v = __shfl_up(depth, o, kWave);
+          if (lane >= o) depth += v;
         }
-        if (isd) last = i;
-        if (m || tk == h.eos_id) stop = min(stop, i);
+        depth += carry;
+        carry = __shfl(depth, kWave - 1, kWave);
       }
+      bool isd = false;
+      if (in && !m) {
+        isd = in_set(tk, s_ids, h.n_delim) && depth <= 0;
+        if (isd && i > 0 && !s_msk[pos - 1] && in_set(s_tok[pos - 1], s_ids + ID_DIGIT, h.n_digit)) isd = false;
+      }
+      const unsigned long long bd = __ballot(isd);
+      const unsigned long long bf = __ballot(in && !m);
+      const unsigned long long bs = __ballot(in && (m || tk == h.eos_id));
+      if (bd) last = i0 + 63 - __clzll((long long)bd);
+      filled += __popcll(bf);
+      if (bs) stop = min(stop, i0 + __ffsll((long long)bs) - 1);
       if (p.delim_flag && i < B) p.delim_flag[pos] = (uint8_t)isd;
     }
-    last = wave_max(last);
-    filled = wave_sum(filled);
-    stop = wave_min(stop);
     if (lane == 0) {
       const int split = last + 1;
       const bool fork = s_role[ln] == 0 && split > 0 &&
