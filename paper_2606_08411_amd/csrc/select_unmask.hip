@@ -67,33 +67,57 @@ __global__ __launch_bounds__(SEL_THREADS) void select_unmask_kernel(SelParams p)
   const int w = tid >> 6;
   const int L = h.L, B = h.B, N = h.N, LB = L * B;
 
-  for (int i = tid; i < LB; i += SEL_THREADS) {
+  // Every input of the first SEL_THREADS positions / rows, the per-lane
+  // limits and the id sets (kernel arguments) is loaded before anything is
+  // stored, so the whole first pass costs one memory round trip (separate
+  // loops would wait for each in turn); larger inputs continue below.
+  {
+    const bool pi = tid < LB, ri = tid < N, li = tid < L;
+    const int tk = pi ? p.tokens[tid] : 0;
+    const uint8_t mk = pi ? p.is_masked[tid] : 0;
+    const int ps = ri ? p.row_pos[tid] : 0;
+    const float cf = ri ? p.conf[tid] : 0.f;
+    const int ag = ri ? p.argmax[tid] : 0;
+    const int bl = li ? h.b_len[tid] : 0;
+    const int kl = li ? h.k_lane[tid] : 0;
+    const int rl = li ? h.role[tid] : 1;
+    const int tl = li ? h.t_lane[tid] : 0;
+    int id = 0;
+    if (tid < ID_DIGIT) id = h.delim[tid];
+    else if (tid < ID_OPEN) id = h.digit[tid - ID_DIGIT];
+    else if (tid < ID_CLOSE) id = h.open[tid - ID_OPEN];
+    else if (tid < ID_ALL) id = h.close[tid - ID_CLOSE];
+    if (pi) {
+      s_tok[tid] = tk;
+      s_msk[tid] = mk;
+    }
+    if (ri) {
+      s_pos[tid] = ps;
+      s_conf[tid] = cf;
+      s_arg[tid] = ag;
+    }
+    if (tid < kSelMaxLanes) {
+      s_lo[tid] = 0;
+      s_hi[tid] = 0;
+      s_cnt[tid] = 0;
+      s_nsel[tid] = 0;
+      s_ndraft[tid] = 0;
+      s_blen[tid] = bl;
+      s_k[tid] = kl;
+      s_role[tid] = rl;
+      s_tlane[tid] = tl;
+    }
+    if (tid < ID_ALL) s_ids[tid] = id;
+  }
+  for (int i = tid + SEL_THREADS; i < LB; i += SEL_THREADS) {
     s_tok[i] = p.tokens[i];
     s_msk[i] = p.is_masked[i];
   }
-  for (int n = tid; n < N; n += SEL_THREADS) {
+  for (int n = tid + SEL_THREADS; n < N; n += SEL_THREADS) {
     s_pos[n] = p.row_pos[n];
     s_conf[n] = p.conf[n];
     s_arg[n] = p.argmax[n];
   }
-  if (tid < kSelMaxLanes) {
-    s_lo[tid] = 0;
-    s_hi[tid] = 0;
-    s_cnt[tid] = 0;
-    s_nsel[tid] = 0;
-    s_blen[tid] = tid < L ? h.b_len[tid] : 0;
-    s_k[tid] = tid < L ? h.k_lane[tid] : 0;
-    s_role[tid] = tid < L ? h.role[tid] : 1;
-    s_tlane[tid] = tid < L ? h.t_lane[tid] : 0;
-    s_ndraft[tid] = 0;
-  }
-  // The per-lane limits and id sets live in the kernel arguments; copied
-  // here in one parallel step, the later phases read them from LDS instead
-  // of issuing dependent scalar loads.
-  if (tid < ID_DIGIT) s_ids[tid] = h.delim[tid];
-  else if (tid < ID_OPEN) s_ids[tid] = h.digit[tid - ID_DIGIT];
-  else if (tid < ID_CLOSE) s_ids[tid] = h.open[tid - ID_OPEN];
-  else if (tid < ID_ALL) s_ids[tid] = h.close[tid - ID_CLOSE];
   __syncthreads();
 
   // Candidates, lane row ranges (row_pos is ascending, so each lane's rows
