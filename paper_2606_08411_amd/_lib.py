@@ -136,6 +136,8 @@ def _host_ids(x):
         key = tuple(int(v) for v in x)
         a = _id_sets.get(key)
         if a is None:
+            if len(_id_sets) >= 64:   # a few fixed sets in practice; stay bounded
+                _id_sets.clear()
             a = _id_sets[key] = np.asarray(key, dtype=np.int32)
         return a
     return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
