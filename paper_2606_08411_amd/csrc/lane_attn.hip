@@ -693,12 +693,13 @@ __global__ __launch_bounds__(256) void prefix_scatter_kernel(const int32_t* idx,
 
 // ------------------------------------------------------------------ host
 static int choose_split(int base_wgs, int total_key_tiles) {
-  // Short grids leave CUs idle: split the key tiles until about 512
-  // workgroups exist (two per CU at two wavefronts per SIMD), keeping at
-  // least 3 key tiles per split, since each split adds partials to merge.
-  // Measured with the merge (MI355X, best in [1, 16]): LLaDA step shape
-  // 4 splits, 21.4 us; Dream 8, 29.1 us; Long 4, 62.8 us (128 us
-  // unsplit); Wide 1, 277 us.
+  // Short grids on the 4-tile kernel leave CUs idle: split the key tiles
+  // until about 512 workgroups exist (two per CU at two wavefronts per
+  // SIMD), keeping at least 3 key tiles per split, since each split adds
+  // partials to merge.  Measured with the merge (MI355X, best in [1, 16]):
+  // Long 4 splits, 62.8 us (128 us unsplit); Wide 1, 277 us (the LLaDA and
+  // Dream step shapes, 4 and 8 splits here, now take the wavefront-split
+  // kernel).
   int s = 1;
   while (s < 16 && base_wgs * s < 512 && total_key_tiles >= 3 * (2 * s)) s *= 2;
   return s;
