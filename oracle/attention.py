@@ -52,13 +52,16 @@ def lane_ancestors(parent):
 def softmax_attend(q, k, v, scale):
     """Plain softmax attention of query rows q [M][D] over keys k, v [S][D].
 
-    Returns (out [M][D], lse [M]) with lse = log sum_k exp(scale * q.k)."""
+    Returns (out [M][D], lse [M]) with lse = log sum_k exp(scale * q.k).
+    Computed in the inputs' precision (fp64 for the oracle; the fp32 twin
+    used only as a CPU timing baseline passes fp32 arrays)."""
     s = scale * (q @ k.T)
     m = s.max(axis=1, keepdims=True)
     e = np.exp(s - m)
     l = e.sum(axis=1, keepdims=True)
     p = e / l
-    assert np.all(np.abs(p.sum(axis=1) - 1.0) < 1e-12), "softmax rows must sum to 1"
+    tol = 1e-12 if p.dtype == np.float64 else 1e-4
+    assert np.all(np.abs(p.sum(axis=1) - 1.0) < tol), "softmax rows must sum to 1"
     return p @ v, (m + np.log(l))[:, 0]
 
 
@@ -184,9 +187,11 @@ def decode_attention(q, k_lane, v_lane, k_pre, v_pre, parent, B,
 
 
 def lane_attention_rows(q, k_lane, v_lane, k_pre, v_pre, parent, B, rows, heads=None,
-                        scale=None):
+                        scale=None, dtype=np.float64):
     """Outputs of selected query rows only, computed one row at a time on the
-    row's own visible key set (for spot checks at full size).
+    row's own visible key set (for spot checks at full size).  dtype is the
+    working precision: fp64 for the oracle; fp32 only for the CPU timing
+    baseline's twin.
     Returns (O [len(rows)][len(heads)][D], LSE [len(rows)][len(heads)])."""
     LB, Hq, D = q.shape
     Hkv = k_lane.shape[1]
@@ -195,16 +200,17 @@ def lane_attention_rows(q, k_lane, v_lane, k_pre, v_pre, parent, B, rows, heads=
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     anc = lane_ancestors(parent)
-    O = np.zeros((len(rows), len(heads), D))
-    LSE = np.zeros((len(rows), len(heads)))
+    O = np.zeros((len(rows), len(heads), D), dtype=dtype)
+    LSE = np.zeros((len(rows), len(heads)), dtype=dtype)
+    cv = lambda x: np.asarray(x, dtype=dtype)
     for a, t in enumerate(rows):
         i = int(t) // B
         blocks = anc[i] + [i]
         for b, h in enumerate(heads):
             kv = h // g
-            kc = np.concatenate([_f64(k_pre[:, kv])] + [_f64(k_lane[j * B:(j + 1) * B, kv]) for j in blocks])
-            vc = np.concatenate([_f64(v_pre[:, kv])] + [_f64(v_lane[j * B:(j + 1) * B, kv]) for j in blocks])
-            o, lse = softmax_attend(_f64(q[t, h])[None, :], kc, vc, scale)
+            kc = np.concatenate([cv(k_pre[:, kv])] + [cv(k_lane[j * B:(j + 1) * B, kv]) for j in blocks])
+            vc = np.concatenate([cv(v_pre[:, kv])] + [cv(v_lane[j * B:(j + 1) * B, kv]) for j in blocks])
+            o, lse = softmax_attend(cv(q[t, h])[None, :], kc, vc, dtype(scale))
             O[a, b] = o[0]
             LSE[a, b] = lse[0]
     return O, LSE

@@ -26,15 +26,16 @@ def _f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
-def logits(hidden, row_idx, W, vocab_chunk=16384):
+def logits(hidden, row_idx, W, vocab_chunk=16384, dtype=np.float64):
     """z = H[row_idx] @ W^T in fp64 ([N][V]).  W is widened to fp64 a chunk
-    of rows at a time only to bound memory."""
-    H = _f64(hidden)[np.asarray(row_idx, dtype=np.int64)]
+    of rows at a time only to bound memory.  (dtype=np.float32 is the fp32
+    twin used only as a CPU timing baseline.)"""
+    H = np.asarray(hidden, dtype=dtype)[np.asarray(row_idx, dtype=np.int64)]
     V = W.shape[0]
-    z = np.empty((H.shape[0], V))
+    z = np.empty((H.shape[0], V), dtype=dtype)
     for c0 in range(0, V, vocab_chunk):
         c1 = min(V, c0 + vocab_chunk)
-        z[:, c0:c1] = H @ _f64(W[c0:c1]).T
+        z[:, c0:c1] = H @ np.asarray(W[c0:c1], dtype=dtype).T
     return z
 
 
@@ -45,10 +46,10 @@ def _allowed(V, suppress, eos_id):
     return allowed
 
 
-def confidence_from_logits(z, suppress_eos=None, eos_id=-1):
+def confidence_from_logits(z, suppress_eos=None, eos_id=-1, dtype=np.float64):
     """Full-softmax form on given logits [N][V].
     Returns dict(conf, argmax, lse, logconf, gap, m)."""
-    z = _f64(z)
+    z = np.asarray(z, dtype=dtype)
     N, V = z.shape
     out = dict(conf=np.zeros(N), argmax=np.zeros(N, dtype=np.int64), lse=np.zeros(N),
                logconf=np.zeros(N), gap=np.full(N, np.inf), m=np.zeros(N))
@@ -69,9 +70,11 @@ def confidence_from_logits(z, suppress_eos=None, eos_id=-1):
     return out
 
 
-def lmhead_confidence_full(hidden, row_idx, W, suppress_eos=None, eos_id=-1):
-    """Full-softmax form over explicit fp64 logits."""
-    return confidence_from_logits(logits(hidden, row_idx, W), suppress_eos, eos_id)
+def lmhead_confidence_full(hidden, row_idx, W, suppress_eos=None, eos_id=-1, dtype=np.float64):
+    """Full-softmax form over explicit fp64 logits (dtype=np.float32: the
+    fp32 twin, a CPU timing baseline only)."""
+    return confidence_from_logits(logits(hidden, row_idx, W, dtype=dtype), suppress_eos, eos_id,
+                                  dtype=dtype)
 
 
 def lmhead_confidence_chunked(hidden, row_idx, W, suppress_eos=None, eos_id=-1,

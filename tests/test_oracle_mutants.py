@@ -44,8 +44,9 @@ MUTANTS = {
          "elif mc == m[n]:\n                s[n] = s[n] + sc\n                idx[n] = ic"),
         ("chunk merge wrong sign", "s[n] = s[n] + sc * np.exp(mc - m[n])", "s[n] = s[n] + sc * np.exp(m[n] - mc)"),
         ("chunked EOS never suppressed", "zn[eos_id - c0] = -np.inf", "pass"),
-        ("gathered rows ignored", "H = _f64(hidden)[np.asarray(row_idx, dtype=np.int64)]\n    V = W.shape[0]\n    z",
-         "H = _f64(hidden)[:len(row_idx)]\n    V = W.shape[0]\n    z"),
+        ("gathered rows ignored",
+         "H = np.asarray(hidden, dtype=dtype)[np.asarray(row_idx, dtype=np.int64)]\n    V = W.shape[0]\n    z",
+         "H = np.asarray(hidden, dtype=dtype)[:len(row_idx)]\n    V = W.shape[0]\n    z"),
         ("lse drops log", "lse = m + np.log(np.exp(zn - m).sum())", "lse = m + np.exp(zn - m).sum()"),
     ],
     "select": [
