@@ -167,7 +167,9 @@ int lane_attn_forward(const al_bf16* q, const al_bf16* k_lane, const al_bf16* v_
  * W        dev [V][d]             bf16 LM-head weight (nn.Linear layout)
  * d        multiple of 8, 8..65536;  n_rows * d < 2^31;  V: 1..2^30
  * suppress_eos dev [N] uint8 or NULL (NULL = no row suppresses EOS)
- * eos_id   in [-1, V); -1 = no EOS id
+ * eos_id   in [-1, V); -1 = no EOS id.  V == 1 with eos_id == 0 and
+ *          suppress_eos given is AL_ERR_SHAPE (a suppressed row would have
+ *          no candidate token).
  * conf, argmax  dev [N] fp32 / int32 out;  lse dev [N] fp32 out or NULL
  * workspace dev, >= lmhead_confidence_workspace_size(N, d, V) bytes of
  *          scratch (per-vocab-tile partial maxima, sums and indices);

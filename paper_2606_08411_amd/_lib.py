@@ -96,6 +96,36 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def _tensor(t, name, dtype, shape=None, min_numel=None, optional=False):
+    """Check a tensor argument before anything reaches the library: its
+    dtype, then its exact shape (shape) or at least min_numel elements (an
+    output buffer of which the call writes a prefix).  Device and layout are
+    checked by _ptr."""
+    if t is None:
+        if optional:
+            return None
+        raise AsyncLaneError(f"{name}: a tensor is required")
+    if not isinstance(t, torch.Tensor):
+        raise AsyncLaneError(f"{name}: torch.Tensor expected, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise AsyncLaneError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(int(x) for x in shape):
+        raise AsyncLaneError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise AsyncLaneError(f"{name}: {t.numel()} elements, at least {min_numel} expected")
+    return t
+
+
+def _same_device(*ts):
+    """Every tensor given is a device tensor, all on one device."""
+    ts = [t for t in ts if t is not None]
+    if any(not t.is_cuda for t in ts):
+        raise AsyncLaneError("device tensor expected")
+    devs = {t.device for t in ts}
+    if len(devs) > 1:
+        raise AsyncLaneError(f"tensors on different devices: {sorted(str(d) for d in devs)}")
+
+
 # torch's raw-handle accessor costs ~0.1 us against ~3 us for
 # torch.cuda.current_stream(); both name the same stream.
 _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
@@ -144,20 +174,40 @@ def _host_ids(x):
 
 
 # ------------------------------------------------------------ workspaces
+# Default workspaces, one per (kind, device, stream): calls on different
+# streams never share one.  A buffer that has to grow is replaced by one at
+# least twice its size and the old one is kept alive (never returned to the
+# allocator), because a launch still in flight may still write to it.  While
+# a HIP graph is being captured the caller must pass its own workspace, so
+# no two graphs (or a graph and eager calls) share one by default.
 _ws_cache: dict = {}
+_ws_retired: list = []
 
 
-def _workspace(kind: str, nbytes: int, device, zeroed: bool):
-    """Device workspace cached per (kind, device); grown on demand."""
+def _workspace(kind: str, nbytes: int, device, stream: int):
     if nbytes == 0:
         return None, 0
-    key = (kind, str(device))
+    if torch.cuda.is_current_stream_capturing():
+        raise AsyncLaneError(
+            f"{kind}: pass workspace= while a HIP graph is being captured (the call needs "
+            f"{nbytes} bytes of workspace)")
+    key = (kind, device.index, int(stream))
     buf = _ws_cache.get(key)
     if buf is None or buf.numel() < nbytes:
-        alloc = torch.zeros if zeroed else torch.empty
-        buf = alloc(max(nbytes, 256), dtype=torch.uint8, device=device)
-        _ws_cache[key] = buf
+        grow = 0 if buf is None else 2 * buf.numel()
+        new = torch.empty(max(nbytes, 256, grow), dtype=torch.uint8, device=device)
+        if buf is not None:
+            _ws_retired.append(buf)
+        _ws_cache[key] = buf = new
     return buf, buf.numel()
+
+
+def _explicit_workspace(ws, device):
+    if not isinstance(ws, torch.Tensor):
+        raise AsyncLaneError("workspace: torch.Tensor expected")
+    if ws.device != device:
+        raise AsyncLaneError(f"workspace on {ws.device}, expected {device}")
+    return ws, ws.numel() * ws.element_size()
 
 
 # ------------------------------------------------------------ entry points
@@ -176,32 +226,60 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
     k_prefix / v_prefix are updated in place when refresh rows are given.
     A refresh-only call (compact cache refresh) passes q = k_lane = v_lane
     = None and parent = [] with refresh rows.  Returns (o, lse, o_ref,
-    lse_ref)."""
+    lse_ref).  Every tensor's dtype and shape is checked before the call."""
     lib = library()
+    bf16, f32 = torch.bfloat16, torch.float32
+    _tensor(k_prefix, "k_prefix", bf16)
+    if k_prefix.dim() != 3:
+        raise AsyncLaneError(f"k_prefix: [P][Hkv][D] expected, got shape {tuple(k_prefix.shape)}")
     P, Hkv, D = k_prefix.shape
+    _tensor(v_prefix, "v_prefix", bf16, (P, Hkv, D))
     L = len(parent)
     par = _host_i32(parent, L, "parent")
     n_ref = 0 if refresh_idx is None else int(refresh_idx.shape[0])
     dev = k_prefix.device
     if L > 0:
-        LB, Hq, _ = q.shape
+        B = int(B)
+        _tensor(q, "q", bf16)
+        if q.dim() != 3 or q.shape[0] != L * B or q.shape[2] != D:
+            raise AsyncLaneError(f"q: [L*B={L * B}][Hq][D={D}] expected, got {tuple(q.shape)}")
+        Hq = int(q.shape[1])
+        LB = L * B
+        _tensor(k_lane, "k_lane", bf16, (LB, Hkv, D))
+        _tensor(v_lane, "v_lane", bf16, (LB, Hkv, D))
         if o is None:
             o = torch.empty_like(q)
         if lse is None and want_lse:
-            lse = torch.empty((LB, Hq), dtype=torch.float32, device=dev)
+            lse = torch.empty((LB, Hq), dtype=f32, device=dev)
+        _tensor(o, "o", bf16, (LB, Hq, D))
+        _tensor(lse, "lse", f32, (LB, Hq), optional=True)
     else:
-        Hq = q_ref.shape[1]
+        if n_ref == 0:
+            raise AsyncLaneError("lane_attn_forward: no lanes and no refresh rows")
+        _tensor(q_ref, "q_ref", bf16)
+        if q_ref.dim() != 3:
+            raise AsyncLaneError(f"q_ref: [n_refresh][Hq][D] expected, got {tuple(q_ref.shape)}")
+        Hq = int(q_ref.shape[1])
         B = 16
     if n_ref:
+        _tensor(refresh_idx, "refresh_idx", torch.int32, (n_ref,))
+        _tensor(q_ref, "q_ref", bf16, (n_ref, Hq, D))
+        _tensor(k_ref, "k_ref", bf16, (n_ref, Hkv, D))
+        _tensor(v_ref, "v_ref", bf16, (n_ref, Hkv, D))
         if o_ref is None:
             o_ref = torch.empty_like(q_ref)
         if lse_ref is None and want_lse:
-            lse_ref = torch.empty((n_ref, Hq), dtype=torch.float32, device=dev)
+            lse_ref = torch.empty((n_ref, Hq), dtype=f32, device=dev)
+        _tensor(o_ref, "o_ref", bf16, (n_ref, Hq, D))
+        _tensor(lse_ref, "lse_ref", f32, (n_ref, Hq), optional=True)
+    _same_device(q, k_lane, v_lane, k_prefix, v_prefix, o, lse, refresh_idx, q_ref, k_ref,
+                 v_ref, o_ref, lse_ref)
     need = int(lib.lane_attn_workspace_size(L, B, P, Hq, Hkv, D, n_ref))
+    if workspace is not None:
+        ws, ws_bytes = _explicit_workspace(workspace, dev)
+    stream = _stream(k_prefix)
     if workspace is None:
-        ws, ws_bytes = _workspace("attn", need, dev, zeroed=False)
-    else:
-        ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
+        ws, ws_bytes = _workspace("attn", need, dev, stream)
     st = lib.lane_attn_forward(
         _ptr(q), _ptr(k_lane), _ptr(v_lane), _ptr(k_prefix), _ptr(v_prefix),
         _np_ptr(par) if L else None,
@@ -209,8 +287,7 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
         _ptr(refresh_idx) if n_ref else None, n_ref,
         _ptr(q_ref) if n_ref else None, _ptr(k_ref) if n_ref else None,
         _ptr(v_ref) if n_ref else None, _ptr(o_ref) if n_ref else None,
-        _ptr(lse_ref) if n_ref else None, _ptr(o), _ptr(lse), _ptr(ws), ws_bytes,
-        _stream(k_prefix))
+        _ptr(lse_ref) if n_ref else None, _ptr(o), _ptr(lse), _ptr(ws), ws_bytes, stream)
     _check(st, "lane_attn_forward")
     return o, lse, o_ref, lse_ref
 
@@ -231,16 +308,23 @@ def lmhead_confidence_workspace_size(N, d, V) -> int:
     return int(library().lmhead_confidence_workspace_size(N, d, V))
 
 
-def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
-                      conf=None, argmax=None, lse=None, want_lse=True, workspace=None):
-    """Per scored row: max softmax probability, its token id and the
-    log-sum-exp over the vocabulary (EOS excluded for suppressed rows).
-    hidden [n_rows][d] and W [V][d] are bf16 device tensors; row_idx is an
-    int32 device tensor (None = every row).  Returns (conf, argmax, lse)."""
-    lib = library()
+def _lmhead_args(hidden, W, row_idx, suppress_eos, conf, argmax, lse, want_lse):
+    """Checks and output allocation shared by the two LM-head calls."""
+    bf16 = torch.bfloat16
+    _tensor(hidden, "hidden", bf16)
+    if hidden.dim() != 2:
+        raise AsyncLaneError(f"hidden: [n_rows][d] expected, got shape {tuple(hidden.shape)}")
     n_rows, d = hidden.shape
-    V = W.shape[0]
-    N = n_rows if row_idx is None else int(row_idx.shape[0])
+    _tensor(W, "W", bf16)
+    if W.dim() != 2 or W.shape[1] != d:
+        raise AsyncLaneError(f"W: [V][d={d}] expected, got shape {tuple(W.shape)}")
+    N = n_rows
+    if row_idx is not None:
+        _tensor(row_idx, "row_idx", torch.int32)
+        if row_idx.dim() != 1:
+            raise AsyncLaneError(f"row_idx: 1-D expected, got shape {tuple(row_idx.shape)}")
+        N = int(row_idx.shape[0])
+    _tensor(suppress_eos, "suppress_eos", torch.uint8, min_numel=N, optional=True)
     dev = hidden.device
     if conf is None:
         conf = torch.empty(N, dtype=torch.float32, device=dev)
@@ -248,16 +332,36 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
         argmax = torch.empty(N, dtype=torch.int32, device=dev)
     if lse is None and want_lse:
         lse = torch.empty(N, dtype=torch.float32, device=dev)
+    _tensor(conf, "conf", torch.float32, min_numel=N)
+    _tensor(argmax, "argmax", torch.int32, min_numel=N)
+    _tensor(lse, "lse", torch.float32, min_numel=N, optional=True)
+    _same_device(hidden, W, row_idx, suppress_eos, conf, argmax, lse)
+    return n_rows, d, int(W.shape[0]), N, conf, argmax, lse
+
+
+def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
+                      conf=None, argmax=None, lse=None, want_lse=True, workspace=None):
+    """Per scored row: max softmax probability, its token id and the
+    log-sum-exp over the vocabulary (EOS excluded for suppressed rows).
+    hidden [n_rows][d] and W [V][d] are bf16 device tensors; row_idx is an
+    int32 device tensor (None = every row).  Output buffers passed in need
+    at least N entries (the first N are written).  Returns (conf, argmax,
+    lse)."""
+    lib = library()
+    n_rows, d, V, N, conf, argmax, lse = _lmhead_args(hidden, W, row_idx, suppress_eos, conf,
+                                                      argmax, lse, want_lse)
     if N == 0:
         return conf, argmax, lse
+    dev = hidden.device
     need = int(lib.lmhead_confidence_workspace_size(N, d, V))
+    if workspace is not None:
+        ws, ws_bytes = _explicit_workspace(workspace, dev)
+    stream = _stream(hidden)
     if workspace is None:
-        ws, ws_bytes = _workspace("lmhead", need, dev, zeroed=False)
-    else:
-        ws, ws_bytes = workspace, workspace.numel() * workspace.element_size()
+        ws, ws_bytes = _workspace("lmhead", need, dev, stream)
     st = lib.lmhead_confidence(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
                                _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
-                               _ptr(lse), _ptr(ws), ws_bytes, _stream(hidden))
+                               _ptr(lse), _ptr(ws), ws_bytes, stream)
     _check(st, "lmhead_confidence")
     return conf, argmax, lse
 
@@ -273,7 +377,17 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
     tensors: unmask_flag, unmasked_pos, still_masked_pos, counts,
     lane_stats, delim_flag."""
     lib = library()
+    L, B = int(L), int(B)
+    _tensor(row_pos, "row_pos", torch.int32)
+    if row_pos.dim() != 1:
+        raise AsyncLaneError(f"row_pos: 1-D expected, got shape {tuple(row_pos.shape)}")
     N = int(row_pos.shape[0])
+    _tensor(conf, "conf", torch.float32, min_numel=N)
+    _tensor(argmax, "argmax", torch.int32, min_numel=N)
+    for t, name, dt in ((tokens, "tokens", torch.int32), (is_masked, "is_masked", torch.uint8)):
+        _tensor(t, name, dt)
+        if t.numel() != L * B:
+            raise AsyncLaneError(f"{name}: {t.numel()} elements, L*B = {L * B} expected")
     dev = tokens.device
     role_h = _host_u8(role, L, "role")
     b_len_h = None if b_len is None else _host_i32(b_len, L, "b_len")
@@ -289,6 +403,14 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
             counts=torch.empty(2, dtype=torch.int32, device=dev),
             lane_stats=torch.empty((L, LANE_STATS), dtype=torch.int32, device=dev),
             delim_flag=torch.empty(L * B, dtype=torch.uint8, device=dev) if with_delim_flag else None)
+    for name, dt, n in (("unmask_flag", torch.uint8, N), ("unmasked_pos", torch.int32, N),
+                        ("still_masked_pos", torch.int32, N), ("counts", torch.int32, 2),
+                        ("lane_stats", torch.int32, L * LANE_STATS)):
+        if name not in out:
+            raise AsyncLaneError(f"out: missing '{name}'")
+        _tensor(out[name], name, dt, min_numel=n)
+    _tensor(out.get("delim_flag"), "delim_flag", torch.uint8, min_numel=L * B, optional=True)
+    _same_device(conf, argmax, row_pos, tokens, is_masked, *out.values())
     st = lib.select_unmask(
         _ptr(conf) if N else None, _ptr(argmax) if N else None, _ptr(row_pos) if N else None, N,
         _ptr(tokens), _ptr(is_masked), L, B, _np_ptr(role_h), _np_ptr(b_len_h), _np_ptr(t_lane_h),

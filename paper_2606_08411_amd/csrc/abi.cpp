@@ -101,18 +101,37 @@ size_t lmhead_confidence_workspace_size(int N, int d, int V) {
   return al::lmhead_workspace_bytes(N, d, V);
 }
 
-int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
-                      const al_bf16* W, int d, int V, const uint8_t* suppress_eos, int eos_id,
-                      float* conf, int32_t* argmax, float* lse, void* workspace,
-                      size_t workspace_bytes, void* stream) {
+// Checks shared by lmhead_confidence and lmhead_confidence_noalloc.  Returns
+// AL_OK with *skip = true for N == 0 (nothing to enqueue).
+static int lmhead_check(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
+                        const al_bf16* W, int d, int V, const uint8_t* suppress_eos, int eos_id,
+                        float* conf, int32_t* argmax, float* lse, bool* skip) {
+  *skip = false;
   if (!lm_shape_ok(N, d, V) || n_rows < 0 || N > n_rows) return AL_ERR_SHAPE;
   if ((long long)n_rows * d >= (1ll << 31)) return AL_ERR_SHAPE;  // 32-bit row offsets
   if (eos_id < -1 || eos_id >= V) return AL_ERR_SHAPE;
-  if (N == 0) return AL_OK;
+  // A suppressed row of a one-token vocabulary whose only id is EOS would
+  // have no candidate token at all.
+  if (V == 1 && eos_id == 0 && suppress_eos) return AL_ERR_SHAPE;
+  if (N == 0) {
+    *skip = true;
+    return AL_OK;
+  }
   if (!hidden || !W || !conf || !argmax) return AL_ERR_NULL;
   if (!aligned16(hidden) || !aligned16(W) || !aligned4(conf) || !aligned4(argmax) ||
       (row_idx && !aligned4(row_idx)) || (lse && !aligned4(lse)))
     return AL_ERR_ALIGN;
+  return AL_OK;
+}
+
+int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
+                      const al_bf16* W, int d, int V, const uint8_t* suppress_eos, int eos_id,
+                      float* conf, int32_t* argmax, float* lse, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  bool skip = false;
+  const int st = lmhead_check(hidden, n_rows, row_idx, N, W, d, V, suppress_eos, eos_id, conf,
+                              argmax, lse, &skip);
+  if (st != AL_OK || skip) return st;
   const size_t need = al::lmhead_workspace_bytes(N, d, V);
   if (!workspace) return AL_ERR_NULL;
   if (workspace_bytes < need) return AL_ERR_WORKSPACE;

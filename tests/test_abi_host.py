@@ -155,3 +155,10 @@ def test_refresh_only_attention_validation(lib):
     assert f(None, None, None, FAKE, FAKE, None, 0, 16, 64, 4, 4, 64, 0.0, None, 0, None, None,
              None, None, None, None, None, None, 0, None) == -2
     assert lib.lane_attn_workspace_size(0, 16, 64, 4, 4, 64, 0) == 0
+
+
+def test_lmhead_one_token_vocabulary(lib):
+    """V = 1 with eos_id = 0 and suppression flags would leave a suppressed
+    row without any candidate: rejected before any launch."""
+    f = lib.lmhead_confidence
+    assert f(FAKE, 4, None, 4, FAKE, 64, 1, FAKE, 0, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2

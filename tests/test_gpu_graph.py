@@ -49,6 +49,12 @@ class _Step:
         self.tok = t["tok0"].clone()
         self.msk = t["msk0"].clone()
         self.sel = None
+        # explicit workspaces: the binding refuses its default ones while a
+        # graph is being captured
+        ws = al.lane_attn_workspace_size(s.L, s.B, s.P, s.Hq, s.Hkv, s.D, s.n_ref)
+        self.ws_attn = torch.empty(max(ws, 16), dtype=torch.uint8, device="cuda")
+        self.ws_lm = torch.empty(al.lmhead_confidence_workspace_size(s.N, s.d, s.V),
+                                 dtype=torch.uint8, device="cuda")
 
     def __call__(self):
         al, s, t = self.al, self.s, self.t
@@ -57,9 +63,10 @@ class _Step:
             ref = dict(refresh_idx=t["ridx"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
                        o_ref=self.o_ref, lse_ref=self.lse_ref)
         al.lane_attn_forward(t["q"], t["kl"], t["vl"], t["kp"], t["vp"], s.parent, s.B,
-                             o=self.o, lse=self.lse, **ref)
+                             o=self.o, lse=self.lse, workspace=self.ws_attn, **ref)
         al.lmhead_confidence(t["hidden"], t["W"], row_idx=t["row_pos"], suppress_eos=t["sup"],
-                             eos_id=s.eos_id, conf=self.conf, argmax=self.arg, lse=self.lm_lse)
+                             eos_id=s.eos_id, conf=self.conf, argmax=self.arg, lse=self.lm_lse,
+                             workspace=self.ws_lm)
         self.sel = al.select_unmask(self.conf, self.arg, t["row_pos"], self.tok, self.msk, s.L,
                                     s.B, s.role, s.b_len, s.t_lane, al.MODE_THRESHOLD, s.tau,
                                     s.fallback_k, delim_ids=s.delim_ids, eos_id=s.eos_id,
@@ -81,7 +88,7 @@ class _Step:
 def test_graph_replays_match_eager(name):
     s, t = _inputs(name, 0)
     st = _Step(s, t)
-    st()                      # eager: allocates the cached workspaces, then the reference
+    st()                      # eager reference
     torch.cuda.synchronize()
     st.reset()
     st()
