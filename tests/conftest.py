@@ -16,14 +16,33 @@ def pytest_configure(config):
 import pytest  # noqa: E402
 
 
+def _say(config, msg):
+    """Write msg to the terminal's stderr with pytest's output capture
+    suspended (fd-level capture would otherwise hold it back until a
+    failure)."""
+    capman = config.pluginmanager.getplugin("capturemanager")
+    if capman is None:
+        sys.stderr.write(msg + "\n")
+        sys.stderr.flush()
+        return
+    with capman.global_and_fixture_disabled():
+        sys.stderr.write(msg + "\n")
+        sys.stderr.flush()
+
+
 @pytest.fixture(autouse=True)
 def _announce_gpu_case(request):
     """Name every GPU test on the real stderr before it touches the device,
     so a run that ends abruptly still shows which case was running."""
     if request.node.get_closest_marker("gpu") is not None:
-        sys.__stderr__.write(f"\n[gpu-case] {request.node.nodeid}\n")
-        sys.__stderr__.flush()
+        _say(request.config, f"[gpu-case] {request.node.nodeid}")
     yield
+
+
+@pytest.fixture
+def report(request):
+    """report(msg): a line in the test log, passing runs included."""
+    return lambda msg: _say(request.config, msg)
 
 
 _STEPS = {}

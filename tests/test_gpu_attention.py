@@ -39,11 +39,18 @@ def _run(step, want_lse=True):
     return out
 
 
-def _sample_rows(step, per_lane=3):
+def _sample_rows(step):
+    """Rows 0, B/2 and B-1 of every lane plus seeded extra rows (6 per lane
+    up to 8 lanes, 4 up to 16, 3 beyond; the oracle computes each row on its
+    own context)."""
+    per_lane = 6 if step.L <= 8 else (4 if step.L <= 16 else 3)
+    g = np.random.default_rng([step.seed, 41])
     rows = []
     for i in range(step.L):
-        for a in sorted(set([0, step.B // 2, step.B - 1][:per_lane])):
-            rows.append(i * step.B + a)
+        pick = {0, step.B // 2, step.B - 1}
+        while len(pick) < min(per_lane, step.B):
+            pick.add(int(g.integers(step.B)))
+        rows += [i * step.B + a for a in sorted(pick)]
     return rows
 
 
@@ -59,9 +66,12 @@ def _check_full(step, out):
         assert np.abs(out["lse_ref"] - ref["lse_ref"]).max() < TOL_LSE
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2])
 @pytest.mark.parametrize("name", ["tiny", "llada", "dream", "long", "wide"])
-def test_attention_workloads(name, step_cache):
-    step = step_cache(name, 0, with_weight=False)
+def test_attention_workloads(name, seed, step_cache):
+    """Each seed draws its own inputs and (Dream, Long, Wide) its own lane
+    tree (Section 3.3: the tree grows by forks, so every shape occurs)."""
+    step = step_cache(name, seed, with_weight=False)
     out = _run(step)
     kp, vp = f32(step.k_pre), f32(step.v_pre)
     if step.n_ref:
@@ -76,7 +86,8 @@ def test_attention_workloads(name, step_cache):
     assert np.abs(out["o"][rows] - o).max() < TOL_O
     assert np.abs(out["lse"][rows] - lse).max() < TOL_LSE
     if step.n_ref:
-        rr = [0, 1, step.n_ref // 2, step.n_ref - 1]
+        rr = sorted({0, 1, step.n_ref // 2, step.n_ref - 1} |
+                    set(np.random.default_rng([seed, 43]).choice(step.n_ref, 12, replace=False).tolist()))
         o_r, l_r = oracle.attention.refresh_attention(f32(step.q_ref)[rr], kp, vp)
         assert np.abs(out["o_ref"][rr] - o_r).max() < TOL_O
         assert np.abs(out["lse_ref"][rr] - l_r).max() < TOL_LSE

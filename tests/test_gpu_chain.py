@@ -1,0 +1,176 @@
+"""The transfer rule end to end (paper Section 3.2, "Lane-local denoising":
+confidence-based transfer inside each lane's valid update region, refine
+lanes without EOS): GPU lmhead_confidence -> GPU select_unmask against the
+fp64 oracle LM head -> oracle selection, on every workload at seeds 0, 1, 2.
+
+Several answers are correct where the fp64 and the fp32 computations may
+order two values differently.  Working in the log domain (logconf = m -
+lse of the oracle), these cases are excluded, counted and printed:
+  (i)   rows whose top-2 logits differ by < 1e-3: the argmax.  A lane with
+        such a row that either side transfers (or drafts) is excluded, since
+        the token written there may differ;
+  (ii)  rows with |logconf - ln tau| < 1e-3 (threshold decision) or, for
+        lookahead rows, |logconf - ln tau_future| < 1e-3: their lane;
+  (iii) lanes whose k-th and (k+1)-th candidates (top-k, or the fallback
+        winner and runner-up) differ by < 1e-3 in logconf: the lane.
+Everything else must match bit for bit: unmask flags, written-back tokens
+and mask bits, the ordered position lists (restricted to the lanes kept),
+lane statistics and delimiter flags.  The LM-head outputs themselves are
+checked on every row: conf within 2e-2, lse within 2e-3, argmax exact
+outside (i), and |logconf_gpu - logconf_oracle| well inside the 1e-3 band,
+which is what makes the exclusions sufficient.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import dev, dev_bf16, f32
+
+pytestmark = pytest.mark.gpu
+BAND = 1e-3
+TOL_CONF = 2e-2
+TOL_LSE = 2e-3
+
+
+
+
+def _gpu_lm(step, W_dev):
+    import paper_2606_08411_amd as al
+    conf, arg, lse = al.lmhead_confidence(dev_bf16(step.hidden), W_dev, row_idx=dev(step.row_pos),
+                                          suppress_eos=dev(step.suppress_eos), eos_id=step.eos_id)
+    torch.cuda.synchronize()
+    return conf, arg, lse
+
+
+def _oracle_lm(step):
+    return oracle.lmhead.lmhead_confidence_full(f32(step.hidden), step.row_pos, f32(step.W),
+                                                step.suppress_eos, step.eos_id)
+
+
+def _rank_excluded(lc, pos, k):
+    """True when the k-th and (k+1)-th of the lane's candidates (logconf
+    descending, position ascending) lie within the band."""
+    if k <= 0 or k >= len(lc):
+        return False
+    order = sorted(range(len(lc)), key=lambda j: (-lc[j], pos[j]))
+    return lc[order[k - 1]] - lc[order[k]] < BAND
+
+
+def _exclusions(step, ref_lm, gpu_flag, ref_flag, mode, fb, k_lane, b_len, tau_future):
+    B, L = step.B, step.L
+    lane = step.row_pos // B
+    lpos = step.row_pos % B
+    lc = ref_lm["logconf"]
+    n_i = n_ii = n_iii = 0
+    excl = np.zeros(L, bool)
+    ln_tau = math.log(step.tau)
+    for l in range(L):
+        rows = np.flatnonzero(lane == l)
+        cand = rows[lpos[rows] < b_len[l]]
+        window = rows[lpos[rows] >= b_len[l]]
+        # (i) argmax near-ties on rows written by either side
+        moved = rows[(gpu_flag[rows] != 0) | (ref_flag[rows] != 0)]
+        if np.any(ref_lm["gap"][moved] < BAND):
+            excl[l] = True
+            n_i += 1
+        # (ii) threshold decisions near tau / tau_future
+        if mode == 0 and np.any(np.abs(lc[cand] - ln_tau) < BAND):
+            excl[l] = True
+            n_ii += 1
+        if tau_future is not None and step.role[l] == synth.ROLE_GEN and len(window) and \
+                np.any(np.abs(lc[window] - math.log(tau_future)) < BAND):
+            excl[l] = True
+            n_ii += 1
+        # (iii) rank near-ties at the cut of top-k or of the fallback
+        if mode == 1:
+            k = min(int(k_lane[l]), len(cand))
+        elif fb > 0 and not np.any(lc[cand] >= ln_tau):
+            k = min(fb, len(cand))
+        else:
+            k = 0
+        if _rank_excluded(list(lc[cand]), list(step.row_pos[cand]), k):
+            excl[l] = True
+            n_iii += 1
+    return excl, (n_i, n_ii, n_iii)
+
+
+def _run_case(step, W_dev, gpu_lm, ref_lm, mode, fb, k_lane, b_len, tau_future, label, report):
+    import paper_2606_08411_amd as al
+    conf, arg, _ = gpu_lm
+    tok_d, msk_d = dev(step.tokens), dev(step.is_masked)
+    out = al.select_unmask(conf, arg, dev(step.row_pos), tok_d, msk_d, step.L, step.B, step.role,
+                           b_len, step.t_lane, mode, step.tau, fb, k_lane, step.delim_ids,
+                           step.eos_id, step.rho_min, step.t_min, tau_future=tau_future)
+    torch.cuda.synchronize()
+    ref = oracle.select.select_unmask(ref_lm["conf"], ref_lm["argmax"], step.row_pos, step.tokens,
+                                      step.is_masked, step.B, step.role, b_len, step.t_lane, mode,
+                                      step.tau, fb, k_lane, step.delim_ids, step.eos_id,
+                                      step.rho_min, step.t_min, tau_future=tau_future)
+    N, B, L = step.N, step.B, step.L
+    g_flag = out["unmask_flag"].cpu().numpy()[:N]
+    excl, counts = _exclusions(step, ref_lm, g_flag, ref["unmask_flag"], mode, fb, k_lane, b_len,
+                               tau_future)
+    keep = ~excl
+    row_keep = keep[step.row_pos // B]
+    pos_keep = np.repeat(keep, B)
+    assert np.array_equal(g_flag[row_keep], ref["unmask_flag"][row_keep]), label
+    assert np.array_equal(tok_d.cpu().numpy()[pos_keep], ref["tokens"][pos_keep]), label
+    assert np.array_equal(msk_d.cpu().numpy()[pos_keep], ref["is_masked"][pos_keep]), label
+    assert np.array_equal(out["lane_stats"].cpu().numpy()[keep], ref["lane_stats"][keep]), label
+    assert np.array_equal(out["delim_flag"].cpu().numpy()[pos_keep], ref["delim_flag"][pos_keep]), label
+    cu, cs = (int(x) for x in out["counts"].cpu().numpy())
+    up = out["unmasked_pos"].cpu().numpy()[:cu]
+    sp = out["still_masked_pos"].cpu().numpy()[:cs]
+    assert np.array_equal(up[keep[up // B]], ref["unmasked_pos"][keep[ref["unmasked_pos"] // B]]), label
+    assert np.array_equal(sp[keep[sp // B]], ref["still_masked_pos"][keep[ref["still_masked_pos"] // B]]), label
+    if keep.all():
+        assert [cu, cs] == list(ref["counts"]), label
+    n_sel = int((ref["unmask_flag"] == 1).sum())
+    n_draft = int((ref["unmask_flag"] == 2).sum())
+    report(f"[{label}] lanes={L} excluded_lanes={int(excl.sum())} (i) argmax={counts[0]} "
+          f"(ii) threshold={counts[1]} (iii) rank={counts[2]}; oracle transfers={n_sel} "
+          f"drafts={n_draft}")
+    return int(excl.sum())
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("name", ["tiny", "llada", "dream", "long", "wide"])
+def test_transfer_rule_chain(name, seed, step_cache, report):
+    step = step_cache(name, seed)
+    W_dev = dev_bf16(step.W)
+    conf, arg, lse = _gpu_lm(step, W_dev)
+    ref_lm = _oracle_lm(step)
+    c, a, ls = conf.cpu().numpy(), arg.cpu().numpy(), lse.cpu().numpy()
+    ok = ref_lm["gap"] >= BAND
+    n_gap = int((~ok).sum())
+    dlog = np.abs((np.log(c.astype(np.float64)) - ref_lm["logconf"])).max()
+    report(f"[{name} seed {seed}] N={step.N} (i) rows with top-2 gap < {BAND}: {n_gap}; "
+          f"max|dconf|={np.abs(c - ref_lm['conf']).max():.2e} max|dlse|="
+          f"{np.abs(ls - ref_lm['lse']).max():.2e} max|dlogconf|={dlog:.2e}")
+    assert np.abs(c - ref_lm["conf"]).max() < TOL_CONF
+    assert np.abs(ls - ref_lm["lse"]).max() < TOL_LSE
+    assert dlog < BAND / 4            # the exclusion band covers the fp32 error
+    assert np.array_equal(a[ok], ref_lm["argmax"][ok])
+    assert n_gap <= max(2, step.N // 50)
+    gpu_lm = (conf, arg, lse)
+    rng = np.random.default_rng([seed, 31])
+    k_lane = rng.integers(0, step.B + 1, step.L).astype(np.int32)
+    b_win = rng.integers(step.B // 2, step.B + 1, step.L).astype(np.int32)
+    cases = [  # mode, fallback_k, k_lane, b_len, tau_future
+        (0, step.fallback_k, None, step.b_len, None),     # the workload's own setting
+        (0, 1, None, step.b_len, None),                   # top-1 fallback
+        (0, 2, None, step.b_len, None),                   # top-2 fallback
+        (1, 0, k_lane, step.b_len, None),                 # top-k per lane
+        (0, 1, None, b_win, 0.5),                         # lookahead window + drafts
+    ]
+    excluded = 0
+    for mode, fb, kl, bl, tf in cases:
+        excluded += _run_case(step, W_dev, gpu_lm, ref_lm, mode, fb, kl, bl, tf,
+                              f"{name} seed {seed} mode {mode} fb {fb} tf {tf}", report)
+    # Near-ties are rare on these inputs; a flood of exclusions would mean the
+    # comparison checks nothing.
+    assert excluded <= max(1, len(cases) * step.L // 8)
