@@ -115,25 +115,46 @@ def device_info():
     return info
 
 
-def cpu_baseline(s, min_seconds=10.0):
+def host_cpu():
+    """(CPUs this process may run on, CPU model string) of the host."""
+    n = len(os.sched_getaffinity(0))
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return n, model
+
+
+def cpu_baseline(s, min_seconds=8.0):
     """The oracle as it stands on a bounded sample of the workload, repeated
     until min_seconds have passed: every attention head of up to 256 lane
     query rows (all of them at the LLaDA shape; otherwise spread over the
     lanes), up to 128 masked rows of the LM head over the whole vocabulary
     (all 77 at the LLaDA shape) and the full selection step; the sampled
-    parts are scaled to the whole step.  Inputs are widened from bf16 before
-    the clock starts (the GPU path also starts with its inputs resident)."""
+    parts are scaled to the whole step.  Timed twice: the fp64 oracle
+    (`value`) and its fp32 twin (the same code at fp32).  Inputs are widened
+    from bf16 before the clock starts (the GPU path also starts with its
+    inputs resident).  BLAS runs on every CPU of the process's affinity
+    set, capped by OMP_NUM_THREADS when that is set (the host's share)."""
     import numpy as np
     import oracle
     import synth
+    affinity, model = host_cpu()
+    threads = affinity
+    if os.environ.get("OMP_NUM_THREADS", "").isdigit():
+        threads = min(threads, int(os.environ["OMP_NUM_THREADS"]))
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([int(x.get("num_threads", 1)) for x in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        limiter = threadpool_limits(limits=threads)
+        used = max([int(x.get("num_threads", 1)) for x in threadpool_info()] or [1])
     except Exception:
-        cores = 1
+        limiter, used = None, threads
     f32 = synth.bf16_bits_to_f32
-    q, kl, vl, kp, vp, H, W = (f32(x) for x in (s.q, s.k_lane, s.v_lane, s.k_pre, s.v_pre,
-                                                s.hidden, s.W))
     LB = s.L * s.B
     if LB <= 256:
         rows = list(range(LB))
@@ -142,37 +163,57 @@ def cpu_baseline(s, min_seconds=10.0):
         rows = sorted({i * s.B + int(a) for i in range(s.L)
                        for a in np.linspace(0, s.B - 1, per).astype(int)})
     nlm = min(128, s.N)
-    t_attn = t_lm = t_sel = 0.0
-    reps = 0
-    t_start = time.perf_counter()
-    while reps == 0 or time.perf_counter() - t_start < min_seconds:
-        t0 = time.perf_counter()
-        oracle.attention.lane_attention_rows(q, kl, vl, kp, vp, s.parent, s.B, rows)
-        t1 = time.perf_counter()
-        ref = oracle.lmhead.lmhead_confidence_full(H, s.row_pos[:nlm], W, s.suppress_eos[:nlm],
-                                                   s.eos_id)
-        t2 = time.perf_counter()
-        conf = np.zeros(s.N)
-        arg = np.zeros(s.N, dtype=np.int64)
-        conf[:nlm], arg[:nlm] = ref["conf"], ref["argmax"]
-        oracle.select.select_unmask(conf, arg, s.row_pos, s.tokens, s.is_masked, s.B, s.role,
-                                    s.b_len, s.t_lane, 0, s.tau, s.fallback_k)
-        t3 = time.perf_counter()
-        t_attn, t_lm, t_sel = t_attn + t1 - t0, t_lm + t2 - t1, t_sel + t3 - t2
-        reps += 1
     depth = depth_of(s.parent)
     f_attn = sum(4.0 * s.D * (s.P + s.B * (depth[r // s.B] + 1)) for r in rows) * s.Hq
     f_lm = 2.0 * nlm * s.d * s.V
-    # Scale each part to the whole step's work, then to TFLOP/s of the step.
-    t_step = (t_attn * attention_flops(s) / f_attn + t_lm * lmhead_flops(s) / f_lm + t_sel) / reps
+
+    def run(dtype):
+        q, kl, vl, kp, vp, H, W = (f32(x).astype(dtype) for x in
+                                   (s.q, s.k_lane, s.v_lane, s.k_pre, s.v_pre, s.hidden, s.W))
+        t_attn = t_lm = t_sel = 0.0
+        reps = 0
+        t_start = time.perf_counter()
+        while reps == 0 or time.perf_counter() - t_start < min_seconds:
+            t0 = time.perf_counter()
+            oracle.attention.lane_attention_rows(q, kl, vl, kp, vp, s.parent, s.B, rows, dtype=dtype)
+            t1 = time.perf_counter()
+            ref = oracle.lmhead.lmhead_confidence_full(H, s.row_pos[:nlm], W, s.suppress_eos[:nlm],
+                                                       s.eos_id, dtype=dtype)
+            t2 = time.perf_counter()
+            conf = np.zeros(s.N)
+            arg = np.zeros(s.N, dtype=np.int64)
+            conf[:nlm], arg[:nlm] = ref["conf"], ref["argmax"]
+            oracle.select.select_unmask(conf, arg, s.row_pos, s.tokens, s.is_masked, s.B, s.role,
+                                        s.b_len, s.t_lane, 0, s.tau, s.fallback_k)
+            t3 = time.perf_counter()
+            t_attn, t_lm, t_sel = t_attn + t1 - t0, t_lm + t2 - t1, t_sel + t3 - t2
+            reps += 1
+        # Each part scaled to the whole step's work, seconds per call.
+        per_call = {"lane_attn_forward": t_attn / reps * attention_flops(s) / f_attn,
+                    "lmhead_confidence": t_lm / reps * lmhead_flops(s) / f_lm,
+                    "select_unmask": t_sel / reps}
+        t_step = sum(per_call.values())
+        return ((attention_flops(s) + lmhead_flops(s)) / t_step / 1e12,
+                {k: round(v, 4) for k, v in per_call.items()}, reps, t_attn + t_lm + t_sel)
+
+    v64, pc64, reps64, sec64 = run(np.float64)
+    v32, pc32, reps32, sec32 = run(np.float32)
+    if limiter is not None:
+        limiter.restore_original_limits()
     return {
-        "value": (attention_flops(s) + lmhead_flops(s)) / t_step / 1e12,
+        "value": v64,
         "unit": "TFLOP/s",
-        "cores": cores,
+        "cores": used,
         "kind": "oracle",
         "sample": f"fp64 oracle: all {s.Hq} heads of {len(rows)} of {LB} lane query rows, "
                   f"{nlm} of {s.N} masked LM-head rows over all {s.V} vocab ids, full selection; "
-                  f"{reps} repetitions in {t_attn + t_lm + t_sel:.1f} s, scaled to one step",
+                  f"{reps64} repetitions in {sec64:.1f} s, scaled to one step",
+        "cpu_model": model,
+        "affinity_cpus": affinity,
+        "blas_threads": used,
+        "seconds_per_call": pc64,
+        "fp32_twin": {"value": v32, "unit": "TFLOP/s", "seconds_per_call": pc32,
+                      "sample": f"the same sample in fp32; {reps32} repetitions in {sec32:.1f} s"},
     }
 
 
@@ -353,13 +394,18 @@ def main():
     msks = [torch.from_numpy(s.is_masked).to(dev) for _ in range(nsteps + args.steps)]
     sel_out = None
 
+    ws_attn = torch.empty(max(16, al.lane_attn_workspace_size(s.L, s.B, s.P, s.Hq, s.Hkv, s.D,
+                                                              n_ref)), dtype=torch.uint8, device=dev)
+    ws_lm = torch.empty(max(16, al.lmhead_confidence_workspace_size(s.N, s.d, s.V)),
+                        dtype=torch.uint8, device=dev)
+
     def attn():
         al.lane_attn_forward(q, kl, vl, kp, vp, s.parent, s.B, o=o, lse=lse, o_ref=o_ref,
-                             lse_ref=lse_ref, **ref_args)
+                             lse_ref=lse_ref, workspace=ws_attn, **ref_args)
 
     def lm():
         al.lmhead_confidence(hidden, W, row_idx=row_pos, suppress_eos=sup, eos_id=s.eos_id,
-                             conf=conf, argmax=arg, lse=lm_lse)
+                             conf=conf, argmax=arg, lse=lm_lse, workspace=ws_lm)
 
     def select(i):
         nonlocal sel_out
@@ -434,7 +480,7 @@ def main():
         def attn_set(k):
             qq, kk, vv, kpp, vpp = sets[k % n_sets]
             al.lane_attn_forward(qq, kk, vv, kpp, vpp, s.parent, s.B, o=o, lse=lse, o_ref=o_ref,
-                                 lse_ref=lse_ref, **ref_args)
+                                 lse_ref=lse_ref, workspace=ws_attn, **ref_args)
 
         for k in range(n_sets):
             attn_set(k)
@@ -545,6 +591,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(s)
+        out["cpu_baseline"]["gpu_over_oracle"] = round(value / out["cpu_baseline"]["value"], 1)
     print(json.dumps(out), flush=True)
 
 
