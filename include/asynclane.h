@@ -26,7 +26,9 @@
  *   pointers are read during the call only (their contents are copied into
  *   kernel arguments before the call returns).
  * - The caller owns every buffer, including workspaces; the library never
- *   allocates, frees or keeps a pointer after a call returns.
+ *   allocates, frees or keeps a pointer after a call returns
+ *   (lmhead_confidence_noalloc keeps its partials in a fixed device array
+ *   of the library instead of a caller workspace).
  * - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *   the call returns before it completes.  Inputs must stay valid until the
  *   stream reaches that point.
@@ -185,6 +187,33 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
                       const uint8_t* suppress_eos, int eos_id,
                       float* conf, int32_t* argmax, float* lse,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * lmhead_confidence_noalloc -- lmhead_confidence without a workspace.
+ *
+ * For callers that cannot allocate device memory at call time: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, results and errors as lmhead_confidence
+ * (bitwise the same outputs: the same kernels run), minus the workspace.
+ * The per-vocab-tile partials go to a fixed device array inside the library
+ * (AL_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends; its
+ * device address is looked up once per device on the first call).  The
+ * call allocates nothing.
+ *
+ * Limit: lmhead_confidence_workspace_size(N, d, V) must not exceed
+ * AL_NOALLOC_SCRATCH_BYTES (with 256 compute units: e.g. N <= 2048 at
+ * V = 126464), else AL_ERR_WORKSPACE before anything is enqueued.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (two streams, or two host threads) race and must be serialised by
+ * the caller.  Nothing in the array needs to start at zero.
+ * ------------------------------------------------------------------------ */
+#define AL_NOALLOC_SCRATCH_BYTES (8u << 20)
+
+int lmhead_confidence_noalloc(const al_bf16* hidden, int n_rows,
+                              const int32_t* row_idx, int N,
+                              const al_bf16* W, int d, int V,
+                              const uint8_t* suppress_eos, int eos_id,
+                              float* conf, int32_t* argmax, float* lse, void* stream);
 
 /* ------------------------------------------------------------------------
  * select_unmask -- per-lane transfer, lookahead drafts, write-back and

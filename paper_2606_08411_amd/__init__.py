@@ -6,6 +6,8 @@ Three calls, backed by hand-written HIP kernels in libasynclane.so:
   over a lane tree, with compact-refresh prefix rows (paper Sections 3.2, 3.4)
 * ``lmhead_confidence``  fused LM-head GEMM + online softmax: per masked
   position the max probability and its token, logits never stored
+  (``lmhead_confidence_noalloc``: the same without a workspace, for callers
+  that cannot allocate)
 * ``select_unmask``      per-lane threshold / top-k transfer, lookahead
   drafts, write-back and lane boundary statistics (eq. split_point,
   eq. fork_condition, ValidBoundary)
@@ -30,6 +32,7 @@ from ._lib import (  # noqa: F401
     lane_attn_workspace_size,
     library,
     lmhead_confidence,
+    lmhead_confidence_noalloc,
     lmhead_confidence_workspace_size,
     select_unmask,
 )

@@ -49,6 +49,8 @@ _SIGNATURES = {
     "al_sched_state": (_i, [_vp, _vp, _vp]),
     "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
                                _sz, _vp]),
+    "lmhead_confidence_noalloc": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp,
+                                       _vp]),
     "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
                            _vp, _vp, _i, _vp, _i, _vp, _i, _vp, _i, _i, _f, _i, _f,
                            _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -363,6 +365,23 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
                                _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
                                _ptr(lse), _ptr(ws), ws_bytes, stream)
     _check(st, "lmhead_confidence")
+    return conf, argmax, lse
+
+
+def lmhead_confidence_noalloc(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
+                              conf=None, argmax=None, lse=None, want_lse=True):
+    """lmhead_confidence without a workspace: the library keeps the partials
+    in a fixed device array of its own (calls that overlap on one GPU race).
+    Pass conf / argmax (/ lse) to allocate nothing at all."""
+    lib = library()
+    n_rows, d, V, N, conf, argmax, lse = _lmhead_args(hidden, W, row_idx, suppress_eos, conf,
+                                                      argmax, lse, want_lse)
+    if N == 0:
+        return conf, argmax, lse
+    st = lib.lmhead_confidence_noalloc(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
+                                       _ptr(suppress_eos), int(eos_id), _ptr(conf),
+                                       _ptr(argmax), _ptr(lse), _stream(hidden))
+    _check(st, "lmhead_confidence_noalloc")
     return conf, argmax, lse
 
 

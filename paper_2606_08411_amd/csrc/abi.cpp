@@ -140,6 +140,21 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx,
                                       argmax, lse, workspace, static_cast<hipStream_t>(stream)));
 }
 
+int lmhead_confidence_noalloc(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
+                              const al_bf16* W, int d, int V, const uint8_t* suppress_eos,
+                              int eos_id, float* conf, int32_t* argmax, float* lse,
+                              void* stream) {
+  bool skip = false;
+  const int st = lmhead_check(hidden, n_rows, row_idx, N, W, d, V, suppress_eos, eos_id, conf,
+                              argmax, lse, &skip);
+  if (st != AL_OK || skip) return st;
+  if (al::lmhead_workspace_bytes(N, d, V) > al::lmhead_scratch_bytes()) return AL_ERR_WORKSPACE;
+  void* scratch_dev = nullptr;  // device address of the library's partials array
+  if (al::lmhead_scratch(&scratch_dev) != hipSuccess) return AL_ERR_HIP;
+  return hip_status(al::launch_lmhead(hidden, row_idx, N, W, d, V, suppress_eos, eos_id, conf,
+                                      argmax, lse, scratch_dev, static_cast<hipStream_t>(stream)));
+}
+
 int select_unmask(const float* conf, const int32_t* argmax, const int32_t* row_pos, int N,
                   int32_t* tokens, uint8_t* is_masked, int L, int B, const uint8_t* role,
                   const int32_t* b_len, const int32_t* t_lane, int mode, float tau, int fallback_k,

@@ -24,6 +24,10 @@ hipError_t launch_lane_attention(const uint16_t* q, const uint16_t* k_lane, cons
 
 // ---- LM head
 size_t lmhead_workspace_bytes(int N, int d, int V);
+// Device address (current device) of the fixed partials array used by
+// lmhead_confidence_noalloc; looked up once per device.
+hipError_t lmhead_scratch(void** out);
+size_t lmhead_scratch_bytes();
 hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N, const uint16_t* W,
                          int d, int V, const uint8_t* sup, int eos_id, float* conf,
                          int32_t* argmax, float* lse, void* ws, hipStream_t stream);

@@ -26,6 +26,10 @@
 //   invalidate the L2 in every workgroup; the separate launch is cheaper.)
 #include <math.h>
 
+#include <atomic>
+#include <mutex>
+
+#include "../../include/asynclane.h"
 #include "common.h"
 #include "launch.h"
 
@@ -428,6 +432,37 @@ static LmLayout lm_layout(int N, int V) {
   L.n_vt = base <= units ? base : units * ((base + units - 1) / units);
   L.total = sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
   return L;
+}
+
+// Partials of lmhead_confidence_noalloc.  In host code `scratch` names a
+// host-side stand-in, not device memory: kernels get the device address
+// that hipGetSymbolAddress returns for the current device (each GPU holds
+// its own copy of the array).
+static __device__ __align__(256) unsigned char scratch[AL_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+static std::atomic<void*> g_scratch_addr[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+size_t lmhead_scratch_bytes() { return sizeof(scratch); }
+
+hipError_t lmhead_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return hipSuccess;
 }
 
 size_t lmhead_workspace_bytes(int N, int d, int V) {

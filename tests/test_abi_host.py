@@ -162,3 +162,24 @@ def test_lmhead_one_token_vocabulary(lib):
     row without any candidate: rejected before any launch."""
     f = lib.lmhead_confidence
     assert f(FAKE, 4, None, 4, FAKE, 64, 1, FAKE, 0, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
+    # without suppression flags, or with another EOS id convention, V = 1 is valid
+    # (checked by the no-alloc twin, whose size limit rejects huge shapes before
+    # touching the device; here the shape is small, so only the rejection runs)
+    g = lib.lmhead_confidence_noalloc
+    assert g(FAKE, 4, None, 4, FAKE, 64, 1, FAKE, 0, FAKE, FAKE, None, None) == -2
+
+
+def test_lmhead_noalloc_validation(lib):
+    """The allocation-free twin applies lmhead_confidence's checks and
+    rejects shapes whose partials exceed its fixed device array with
+    AL_ERR_WORKSPACE, before any device call."""
+    g = lib.lmhead_confidence_noalloc
+    assert g(FAKE, 10, None, 5, FAKE, 12, 100, None, -1, FAKE, FAKE, None, None) == -2
+    assert g(None, 10, None, 5, FAKE, 64, 100, None, -1, FAKE, FAKE, None, None) == -1
+    assert g(FAKE, 10, None, 5, FAKE, 64, 100, None, -1, ctypes.c_void_p((1 << 20) + 2), FAKE,
+             None, None) == -5
+    assert g(FAKE, 10, None, 0, FAKE, 64, 100, None, -1, None, None, None, None) == 0
+    limit = 8 << 20
+    N, V = 30000, 1 << 30
+    assert lib.lmhead_confidence_workspace_size(N, 64, V) > limit
+    assert g(FAKE, N, None, N, FAKE, 64, V, None, -1, FAKE, FAKE, None, None) == -4

@@ -62,7 +62,7 @@ def _lm_args(n=8, d=64, V=100):
                 row_idx=torch.arange(n, dtype=torch.int32))
 
 
-@pytest.mark.parametrize("fn", [al.lmhead_confidence])
+@pytest.mark.parametrize("fn", [al.lmhead_confidence, al.lmhead_confidence_noalloc])
 @pytest.mark.parametrize("key,bad,msg", [
     ("hidden", torch.zeros(8, 64, dtype=torch.float32), "hidden: dtype"),
     ("hidden", torch.zeros(8, 64, 1, dtype=bf16), "hidden:"),
@@ -85,6 +85,8 @@ def test_lmhead_rejects(fn, key, bad, msg):
 def test_lmhead_host_tensors_rejected():
     with pytest.raises(AsyncLaneError, match="device tensor expected"):
         al.lmhead_confidence(**_lm_args())
+    with pytest.raises(AsyncLaneError, match="device tensor expected"):
+        al.lmhead_confidence_noalloc(**_lm_args())
 
 
 def _sel_args(L=2, B=8, N=5):
