@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-reps", type=int, default=50)
+    ap.add_argument("--w-layout", default="packed", choices=["packed", "plain"],
+                    help="LM-head weight layout of the timed step: the one-time packed copy "
+                         "(lmhead_pack_weight, made before timing, like a model load) or W as given")
     ap.add_argument("--quick", action="store_true",
                     help="skip the distribution, cold-input and graph passes (profiler runs)")
     ap.add_argument("--decode", action="store_true",
@@ -89,16 +92,18 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(config):
+def measured_traffic(config, layout):
     """HBM bytes per LM-head call (both kernels) from the committed
-    rocprofv3 counter summary, or None when it is missing or was taken on
-    another version of the kernel source."""
+    rocprofv3 counter summary, or None when it is missing, was taken on
+    another version of the kernel source or on the other weight layout."""
     path = os.path.join(ROOT, "profiles", f"lmhead_confidence_{config}_pmc.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
     if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    if rec.get("w_layout", "plain") != layout:
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -403,9 +408,20 @@ def main():
         al.lane_attn_forward(q, kl, vl, kp, vp, s.parent, s.B, o=o, lse=lse, o_ref=o_ref,
                              lse_ref=lse_ref, workspace=ws_attn, **ref_args)
 
-    def lm():
+    # The packed weight is made once, outside the timed region: weights do
+    # not change between decode steps.
+    W_packed = al.lmhead_pack_weight(W) if args.w_layout == "packed" else None
+
+    def lm_plain():
         al.lmhead_confidence(hidden, W, row_idx=row_pos, suppress_eos=sup, eos_id=s.eos_id,
                              conf=conf, argmax=arg, lse=lm_lse, workspace=ws_lm)
+
+    def lm_packed():
+        al.lmhead_confidence_packed(hidden, W_packed, s.V, row_idx=row_pos, suppress_eos=sup,
+                                    eos_id=s.eos_id, conf=conf, argmax=arg, lse=lm_lse,
+                                    workspace=ws_lm)
+
+    lm = lm_packed if W_packed is not None else lm_plain
 
     def select(i):
         nonlocal sel_out
@@ -447,6 +463,7 @@ def main():
     reps = args.kernel_reps
     t_attn = timed(attn, reps)
     t_lm = timed(lm, reps)
+    t_lm_other = timed(lm_plain, reps) if W_packed is not None else None
     t_sel = timed(lambda: select(nsteps - 1), reps)
 
     def pct(xs):
@@ -553,7 +570,7 @@ def main():
     f_attn, f_lm = attention_flops(s), lmhead_flops(s)
     value = (f_attn + f_lm) / (ms_step * 1e-3) / 1e12
     lm_gbs = lmhead_bytes(s) / (t_lm * 1e-3) / 1e9
-    traffic = measured_traffic(args.config)
+    traffic = measured_traffic(args.config, args.w_layout)
     out = {
         "metric": "lane-attn + fused LM-head TFLOP/s (MFMA util %), masked positions scored/s",
         "value": round(value, 2),
@@ -576,11 +593,14 @@ def main():
         "lane_tokens_per_s": round(s.L * s.B / (ms_step * 1e-3), 1),
         "per_call_ms": {"lane_attn_forward": round(t_attn, 4), "lmhead_confidence": round(t_lm, 4),
                         "select_unmask": round(t_sel, 4)},
+        "lm_weight_layout": args.w_layout,
+        "lmhead_plain_weight_ms": None if t_lm_other is None else round(t_lm_other, 4),
         **extras,
         "attention_tflops": round(f_attn / (t_attn * 1e-3) / 1e12, 2),
         "lmhead_tflops": round(f_lm / (t_lm * 1e-3) / 1e12, 2),
         "roofline": {
-            "kernel": "lmhead_confidence (lmhead_partial_kernel + lmhead_merge_kernel)",
+            "kernel": ("lmhead_confidence_packed" if W_packed is not None else "lmhead_confidence")
+                      + " (lmhead_partial_kernel + lmhead_merge_kernel)",
             "bound": "hbm",
             "achieved": round(lm_gbs, 1),
             "peak": PEAK_HBM_GBS,

@@ -189,6 +189,43 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows,
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Packed LM-head weight: lmhead_pack_weight + lmhead_confidence_packed.
+ *
+ * The same computation as lmhead_confidence (Section 3.2), reading W from a
+ * one-time repacked copy (weights do not change between decode steps, so
+ * the copy is made once, e.g. at model load).  Layout: W is cut into
+ * 32-row units u = v / 32 and 64-element K chunks c = k / 64; block (c, u)
+ * holds 4 x 64 x 8 elements in the order the kernel's registers take them
+ * (step s = (k % 64) / 16, lane l = 32 * ((k % 16) / 8) + v % 32, element
+ * k % 8), and blocks are stored K-chunk-major: element offset
+ *     (((c * ceil(V/32) + u) * 4 + s) * 64 + l) * 8 + k % 8.
+ * Rows past V and K past d are zero.  Reading W chunk by chunk across the
+ * whole vocabulary this way is a near-linear stream of HBM.
+ *
+ * lmhead_packed_weight_size returns the bytes of the packed copy
+ * (ceil(d/64)*64 * ceil(V/32)*32 * 2), 0 for bad arguments.
+ * lmhead_pack_weight: W dev [V][d] in, W_packed dev out (packed_bytes >=
+ * that size, else AL_ERR_WORKSPACE); d, V as for lmhead_confidence.
+ * lmhead_confidence_packed: arguments, results and errors of
+ * lmhead_confidence with W_packed in place of W; the workspace size is
+ * lmhead_confidence_workspace_size(N, d, V).  Results equal
+ * lmhead_confidence's within rounding (the vocabulary is tiled in 32-row
+ * units, so the fp32 sums are grouped and ordered differently); argmax
+ * ties still go to the lowest id.
+ * ------------------------------------------------------------------------ */
+size_t lmhead_packed_weight_size(int d, int V);
+
+int lmhead_pack_weight(const al_bf16* W, int d, int V, al_bf16* W_packed, size_t packed_bytes,
+                       void* stream);
+
+int lmhead_confidence_packed(const al_bf16* hidden, int n_rows,
+                             const int32_t* row_idx, int N,
+                             const al_bf16* W_packed, int d, int V,
+                             const uint8_t* suppress_eos, int eos_id,
+                             float* conf, int32_t* argmax, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * lmhead_confidence_noalloc -- lmhead_confidence without a workspace.
  *
  * For callers that cannot allocate device memory at call time: code being

@@ -7,7 +7,9 @@ Three calls, backed by hand-written HIP kernels in libasynclane.so:
 * ``lmhead_confidence``  fused LM-head GEMM + online softmax: per masked
   position the max probability and its token, logits never stored
   (``lmhead_confidence_noalloc``: the same without a workspace, for callers
-  that cannot allocate)
+  that cannot allocate; ``lmhead_pack_weight`` + ``lmhead_confidence_packed``:
+  the same from a one-time repacked copy of W that streams like a linear
+  read)
 * ``select_unmask``      per-lane threshold / top-k transfer, lookahead
   drafts, write-back and lane boundary statistics (eq. split_point,
   eq. fork_condition, ValidBoundary)
@@ -33,6 +35,9 @@ from ._lib import (  # noqa: F401
     library,
     lmhead_confidence,
     lmhead_confidence_noalloc,
+    lmhead_confidence_packed,
+    lmhead_pack_weight,
+    lmhead_packed_weight_size,
     lmhead_confidence_workspace_size,
     select_unmask,
 )

@@ -49,6 +49,10 @@ _SIGNATURES = {
     "al_sched_state": (_i, [_vp, _vp, _vp]),
     "lmhead_confidence": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
                                _sz, _vp]),
+    "lmhead_packed_weight_size": (_sz, [_i, _i]),
+    "lmhead_pack_weight": (_i, [_vp, _i, _i, _vp, _sz, _vp]),
+    "lmhead_confidence_packed": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp, _vp,
+                                      _sz, _vp]),
     "lmhead_confidence_noalloc": (_i, [_vp, _i, _vp, _i, _vp, _i, _i, _vp, _i, _vp, _vp, _vp,
                                        _vp]),
     "select_unmask": (_i, [_vp, _vp, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _vp, _i, _f, _i,
@@ -365,6 +369,63 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
                                _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
                                _ptr(lse), _ptr(ws), ws_bytes, stream)
     _check(st, "lmhead_confidence")
+    return conf, argmax, lse
+
+
+def lmhead_packed_weight_size(d, V) -> int:
+    return int(library().lmhead_packed_weight_size(int(d), int(V)))
+
+
+def lmhead_pack_weight(W, out=None):
+    """One-time repack of the LM-head weight W [V][d] (bf16, device) into
+    the layout lmhead_confidence_packed streams.  Returns a flat bf16 device
+    tensor (or fills `out`)."""
+    lib = library()
+    _tensor(W, "W", torch.bfloat16)
+    if W.dim() != 2:
+        raise AsyncLaneError(f"W: [V][d] expected, got shape {tuple(W.shape)}")
+    V, d = (int(x) for x in W.shape)
+    nbytes = int(lib.lmhead_packed_weight_size(d, V))
+    if nbytes == 0:
+        raise AsyncLaneError(f"W: unsupported shape {tuple(W.shape)}")
+    if out is None:
+        out = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=W.device)
+    _tensor(out, "out", torch.bfloat16, min_numel=nbytes // 2)
+    _same_device(W, out)
+    st = lib.lmhead_pack_weight(_ptr(W), d, V, _ptr(out), out.numel() * 2, _stream(W))
+    _check(st, "lmhead_pack_weight")
+    return out
+
+
+def lmhead_confidence_packed(hidden, W_packed, V, row_idx=None, suppress_eos=None, eos_id=-1,
+                             conf=None, argmax=None, lse=None, want_lse=True, workspace=None):
+    """lmhead_confidence reading the weight from lmhead_pack_weight's copy
+    (V = vocabulary size of the original W; d is hidden's width)."""
+    lib = library()
+    _tensor(hidden, "hidden", torch.bfloat16)
+    if hidden.dim() != 2:
+        raise AsyncLaneError(f"hidden: [n_rows][d] expected, got shape {tuple(hidden.shape)}")
+    d = int(hidden.shape[1])
+    V = int(V)
+    nbytes = int(lib.lmhead_packed_weight_size(d, V))
+    _tensor(W_packed, "W_packed", torch.bfloat16, min_numel=max(nbytes // 2, 1))
+    # the shared checks see W_packed as a [1][d] weight (its dtype and device)
+    n_rows, d, _, N, conf, argmax, lse = _lmhead_args(hidden, W_packed.view(-1)[:d].view(1, d),
+                                                      row_idx, suppress_eos, conf, argmax, lse,
+                                                      want_lse)
+    if N == 0:
+        return conf, argmax, lse
+    dev = hidden.device
+    need = int(lib.lmhead_confidence_workspace_size(N, d, V))
+    if workspace is not None:
+        ws, ws_bytes = _explicit_workspace(workspace, dev)
+    stream = _stream(hidden)
+    if workspace is None:
+        ws, ws_bytes = _workspace("lmhead", need, dev, stream)
+    st = lib.lmhead_confidence_packed(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W_packed), d, V,
+                                      _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
+                                      _ptr(lse), _ptr(ws), ws_bytes, stream)
+    _check(st, "lmhead_confidence_packed")
     return conf, argmax, lse
 
 

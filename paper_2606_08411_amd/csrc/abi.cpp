@@ -140,6 +140,37 @@ int lmhead_confidence(const al_bf16* hidden, int n_rows, const int32_t* row_idx,
                                       argmax, lse, workspace, static_cast<hipStream_t>(stream)));
 }
 
+size_t lmhead_packed_weight_size(int d, int V) {
+  if (!lm_shape_ok(1, d, V)) return 0;
+  return al::lmhead_packed_bytes(d, V);
+}
+
+int lmhead_pack_weight(const al_bf16* W, int d, int V, al_bf16* W_packed, size_t packed_bytes,
+                       void* stream) {
+  if (!lm_shape_ok(1, d, V)) return AL_ERR_SHAPE;
+  if (!W || !W_packed) return AL_ERR_NULL;
+  if (!aligned16(W) || !aligned16(W_packed)) return AL_ERR_ALIGN;
+  if (packed_bytes < al::lmhead_packed_bytes(d, V)) return AL_ERR_WORKSPACE;
+  return hip_status(al::launch_lmhead_pack(W, d, V, W_packed, static_cast<hipStream_t>(stream)));
+}
+
+int lmhead_confidence_packed(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
+                             const al_bf16* W_packed, int d, int V, const uint8_t* suppress_eos,
+                             int eos_id, float* conf, int32_t* argmax, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  bool skip = false;
+  const int st = lmhead_check(hidden, n_rows, row_idx, N, W_packed, d, V, suppress_eos, eos_id,
+                              conf, argmax, lse, &skip);
+  if (st != AL_OK || skip) return st;
+  const size_t need = al::lmhead_workspace_bytes(N, d, V);
+  if (!workspace) return AL_ERR_NULL;
+  if (workspace_bytes < need) return AL_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return AL_ERR_ALIGN;
+  return hip_status(al::launch_lmhead(hidden, row_idx, N, W_packed, d, V, suppress_eos, eos_id,
+                                      conf, argmax, lse, workspace,
+                                      static_cast<hipStream_t>(stream), true));
+}
+
 int lmhead_confidence_noalloc(const al_bf16* hidden, int n_rows, const int32_t* row_idx, int N,
                               const al_bf16* W, int d, int V, const uint8_t* suppress_eos,
                               int eos_id, float* conf, int32_t* argmax, float* lse,

@@ -28,9 +28,13 @@ size_t lmhead_workspace_bytes(int N, int d, int V);
 // lmhead_confidence_noalloc; looked up once per device.
 hipError_t lmhead_scratch(void** out);
 size_t lmhead_scratch_bytes();
+// packed: W is in the layout lmhead_pack_weight writes.
 hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N, const uint16_t* W,
                          int d, int V, const uint8_t* sup, int eos_id, float* conf,
-                         int32_t* argmax, float* lse, void* ws, hipStream_t stream);
+                         int32_t* argmax, float* lse, void* ws, hipStream_t stream,
+                         bool packed = false);
+size_t lmhead_packed_bytes(int d, int V);
+hipError_t launch_lmhead_pack(const uint16_t* W, int d, int V, uint16_t* Wp, hipStream_t stream);
 
 // ---- selection
 constexpr int kSelMaxPositions = 8192;

@@ -54,9 +54,24 @@ struct LmParams {
   const uint8_t* sup;
   LmPartial* part;  // [n_nt][nt_cols][n_vt]: a row's partials are contiguous
   int N, d, V, eos_id;
-  // Vocab tile vt covers rows [vt*V/n_vt, (vt+1)*V/n_vt) (<= 32*RT*WAVES rows).
+  // Plain W: vocab tile vt covers rows [vt*V/n_vt, (vt+1)*V/n_vt) (<= 32*RT*WAVES
+  // rows).  Packed W: it covers the 32-row units [vt*n_hg/n_vt, (vt+1)*n_hg/n_vt).
   int n_vt, n_nt, nt_cols, tiles_total, tiles_per_xcd;
+  int n_hg;  // packed W: 32-row units, ceil(V / 32)
 };
+
+// Packed W layout (lmhead_pack_weight).  W is cut into 32-row units u =
+// v / 32 and 64-element K chunks c = k / 64.  Inside a (c, u) block the
+// elements sit exactly as one wavefront's A-operand loads take them: 4
+// MFMA k-steps s of 64 lanes x 8 elements, lane l = 32 h + r holding row
+// 32u + r, K elements 64c + 16s + 8h .. +8.  Blocks are ordered K-chunk
+// major, (c * n_hg + u): while the workgroups stream their tiles in step,
+// the chip reads one contiguous window of ~V * 128 bytes per chunk, like a
+// linear read, instead of 128-byte pieces of every row.  Rows past V and
+// K past d are zero.
+__device__ __host__ __forceinline__ size_t packed_offset(int c, int u, int s, int l, int n_hg) {
+  return ((((size_t)c * n_hg + u) * 4 + s) * 64 + l) * 8;
+}
 
 // Merge (m2, s2, i2) into (m, s, i): max, rescaled sum, lowest index on ties.
 // Commutative, so lanes that exchange states obtain identical bits.
@@ -96,9 +111,12 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 //   steps, and 256*RT vocab rows per workgroup keep the hidden-chunk
 //   traffic at NT/(256*RT) of the W traffic.
 // * Two wavefronts per SIMD: the accumulators take 16*NF*RT registers.
-template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, bool ROT>
+// PACKED: W in the packed layout above (KC = 64, no K rotation: the
+// K-chunk-major order already spreads the reads evenly).
+template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, bool ROT, bool PACKED>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
+  static_assert(!PACKED || (KC == 64 && !ROT), "packed W: 64-element chunks, natural K order");
   constexpr int THREADS = WAVES * 64;
   constexpr int VT = 32 * RT * WAVES;            // vocab rows per workgroup
   constexpr int STEPS = KC / 16;                 // MFMA k-steps per chunk
@@ -129,17 +147,32 @@ void lmhead_partial_kernel(LmParams p) {
   const int r32 = lane & 31;
   const int h = lane >> 5;
   const int d = p.d;
-  const int vb = (int)((long long)vt * p.V / p.n_vt);
-  const int ve = (int)((long long)(vt + 1) * p.V / p.n_vt);
+  int vb, ve, ub = 0, ue = 0;
+  if (PACKED) {
+    ub = (int)((long long)vt * p.n_hg / p.n_vt);
+    ue = (int)((long long)(vt + 1) * p.n_hg / p.n_vt);
+    vb = ub * 32;
+    ve = min(p.V, ue * 32);
+  } else {
+    vb = (int)((long long)vt * p.V / p.n_vt);
+    ve = (int)((long long)(vt + 1) * p.V / p.n_vt);
+  }
   const int v0 = vb + w * 32 * RT;
   const int n0 = nt * p.nt_cols;
   const int ncols = min(NT, p.N - n0);
 
   // Rows past the tile read its last row (cache hits; dropped in the
-  // epilogue).
+  // epilogue).  Packed: wrow[q] is this lane's element of unit u, chunk 0,
+  // step 0; chunk c, step s adds c * n_hg * 2048 + s * 512.
   const uint16_t* wrow[RT];
 #pragma unroll
-  for (int q = 0; q < RT; ++q) wrow[q] = p.W + (size_t)min(v0 + 32 * q + r32, ve - 1) * d;
+  for (int q = 0; q < RT; ++q) {
+    if (PACKED)
+      wrow[q] = p.W + packed_offset(0, min(ub + w * RT + q, ue - 1), 0, lane, p.n_hg);
+    else
+      wrow[q] = p.W + (size_t)min(v0 + 32 * q + r32, ve - 1) * d;
+  }
+  const size_t wchunk = (size_t)p.n_hg * 2048;   // packed: elements per K chunk
   // Hidden staging: segment i of this thread is row hrow0 + i * RSTEP of
   // the column tile, at K offset hk of the staged block.  Only rows < ncols
   // are loaded and stored each block; rows ncols..NT-1 (read by the MFMAs
@@ -175,6 +208,7 @@ void lmhead_partial_kernel(LmParams p) {
   constexpr int RING = PF + 1;   // W register slots (chunks)
   bf16x8 wr[RING][RT * STEPS], hr[HREG];
   auto load_w1 = [&](int q, int kc, int s) {
+    if (PACKED) return load_bf16x8(wrow[q] + (size_t)(kc >> 6) * wchunk + s * 512);
     const int k = kc + s * 16 + h * 8;
     if (RAGGED) return load_bf16x8(wrow[q] + (k < d ? k : 0));
     return load_bf16x8(wrow[q] + k);
@@ -415,7 +449,9 @@ static int lm_cu_count() {
   return cached[dev];
 }
 
-static LmLayout lm_layout(int N, int V) {
+// Packed W is tiled in whole 32-row units (a tile holds up to RT * 8 of
+// them), plain W in rows; both balance the tiles over the CUs the same way.
+static LmLayout lm_layout(int N, int V, bool packed) {
   LmLayout L{};
   const int frags = N > 0 ? (N + 31) / 32 : 1;
   L.n_nt = N > 0 ? (frags + LM_MAX_NF - 1) / LM_MAX_NF : 0;
@@ -427,7 +463,8 @@ static LmLayout lm_layout(int N, int V) {
   // round is not partly empty (V = 152064: 594 full tiles would take 3
   // rounds at 77% use; 768 tiles of 198 rows take 3 even rounds).
   const int vt_rows = lm_vt(L.nf);
-  const int base = (V + vt_rows - 1) / vt_rows;
+  const int base = packed ? ((V + 31) / 32 + vt_rows / 32 - 1) / (vt_rows / 32)
+                          : (V + vt_rows - 1) / vt_rows;
   const int units = lm_cu_count();
   L.n_vt = base <= units ? base : units * ((base + units - 1) / units);
   L.total = sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
@@ -465,18 +502,50 @@ hipError_t lmhead_scratch(void** out) {
   return hipSuccess;
 }
 
+// Either layout's partials fit (one size query serves both entry points).
 size_t lmhead_workspace_bytes(int N, int d, int V) {
   (void)d;
   if (N <= 0 || V <= 0) return 0;
-  return lm_layout(N, V).total;
+  const size_t a = lm_layout(N, V, false).total, b = lm_layout(N, V, true).total;
+  return a > b ? a : b;
+}
+
+size_t lmhead_packed_bytes(int d, int V) {
+  return (size_t)((d + 63) / 64) * 64 * (size_t)((V + 31) / 32) * 32 * sizeof(uint16_t);
+}
+
+// One 16-byte segment per thread and step: segment o of the packed buffer
+// is lane l = o % 64, step s = (o / 64) % 4 of block (c, u) = o / 256.
+__global__ __launch_bounds__(256) void lmhead_pack_kernel(const uint16_t* W, int d, int V,
+                                                          int n_hg, long long n_seg, uint16_t* Wp) {
+  for (long long o = (long long)blockIdx.x * 256 + threadIdx.x; o < n_seg;
+       o += (long long)gridDim.x * 256) {
+    const int l = (int)(o & 63);
+    const int st = (int)((o >> 6) & 3);
+    const long long blk = o >> 8;
+    const int u = (int)(blk % n_hg);
+    const int c = (int)(blk / n_hg);
+    const int v = u * 32 + (l & 31);
+    const int k = c * 64 + st * 16 + (l >> 5) * 8;
+    i32x4 val = {0, 0, 0, 0};
+    if (v < V && k < d) val = *reinterpret_cast<const i32x4*>(W + (size_t)v * d + k);
+    reinterpret_cast<i32x4*>(Wp)[o] = val;
+  }
+}
+
+hipError_t launch_lmhead_pack(const uint16_t* W, int d, int V, uint16_t* Wp, hipStream_t stream) {
+  const int n_hg = (V + 31) / 32;
+  const long long n_seg = (long long)((d + 63) / 64) * n_hg * 256;
+  hipLaunchKernelGGL(lmhead_pack_kernel, dim3(8192), dim3(256), 0, stream, W, d, V, n_hg, n_seg, Wp);
+  return hipGetLastError();
 }
 
 hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
                          const uint16_t* W, int d, int V, const uint8_t* sup, int eos_id,
                          float* conf, int32_t* argmax, float* lse, void* ws,
-                         hipStream_t stream) {
+                         hipStream_t stream, bool packed) {
   if (N <= 0) return hipSuccess;
-  const LmLayout L = lm_layout(N, V);
+  const LmLayout L = lm_layout(N, V, packed);
   LmParams p{};
   p.hidden = hidden;
   p.row_idx = row_idx;
@@ -492,16 +561,20 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.nt_cols = L.nt_cols;
   p.tiles_total = L.n_vt * L.n_nt;
   p.tiles_per_xcd = (p.tiles_total + 7) / 8;
+  p.n_hg = (V + 31) / 32;
   const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
   // The plain kernel assumes d % (KC * SC) == 0; other d take the RAGGED variant.
+#define AL_LM_LAUNCH(F, RG, PK)                                                               \
+  hipLaunchKernelGGL((lmhead_partial_kernel<F, RG, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), \
+                                            !(PK) && lm_rt(F) == 2, PK>),                     \
+                     grid, block, 0, stream, p)
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
-    if (d % (LM_KC * lm_sc(F)) != 0)                                                          \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, true, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_rt(F) == 2>), \
-                         grid, block, 0, stream, p);                                          \
-    else                                                                                      \
-      hipLaunchKernelGGL((lmhead_partial_kernel<F, false, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), lm_rt(F) == 2>), \
-                         grid, block, 0, stream, p);                                          \
+    if (d % (LM_KC * lm_sc(F)) != 0) {                                                        \
+      if (packed) AL_LM_LAUNCH(F, true, true); else AL_LM_LAUNCH(F, true, false);             \
+    } else {                                                                                  \
+      if (packed) AL_LM_LAUNCH(F, false, true); else AL_LM_LAUNCH(F, false, false);           \
+    }                                                                                         \
     break;
   switch (L.nf) {
     AL_LM_CASE(1)
@@ -514,6 +587,7 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
       AL_LM_CASE(7)
   }
 #undef AL_LM_CASE
+#undef AL_LM_LAUNCH
   hipLaunchKernelGGL(lmhead_merge_kernel, dim3(N), dim3(LM_MERGE_THREADS), 0, stream, p.part, N,
                      L.n_vt, L.nt_cols, conf, argmax, lse);
   return hipGetLastError();

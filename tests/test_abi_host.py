@@ -183,3 +183,20 @@ def test_lmhead_noalloc_validation(lib):
     N, V = 30000, 1 << 30
     assert lib.lmhead_confidence_workspace_size(N, 64, V) > limit
     assert g(FAKE, N, None, N, FAKE, 64, V, None, -1, FAKE, FAKE, None, None) == -4
+
+
+def test_lmhead_packed_validation(lib):
+    size = lib.lmhead_packed_weight_size
+    assert size(4096, 126464) == 4096 * 126464 * 2
+    assert size(200, 1000) == 256 * 1024 * 2          # K padded to 64, rows to 32
+    assert size(12, 100) == 0                          # d % 8
+    pack = lib.lmhead_pack_weight
+    assert pack(FAKE, 12, 100, FAKE, 1 << 30, None) == -2
+    assert pack(None, 64, 100, FAKE, 1 << 30, None) == -1
+    assert pack(FAKE, 64, 100, ctypes.c_void_p((1 << 20) + 4), 1 << 30, None) == -5
+    assert pack(FAKE, 64, 100, FAKE, size(64, 100) - 1, None) == -4
+    f = lib.lmhead_confidence_packed
+    assert f(FAKE, 10, None, 5, FAKE, 12, 100, None, -1, FAKE, FAKE, None, FAKE, 1 << 30, None) == -2
+    assert f(None, 10, None, 5, FAKE, 64, 100, None, -1, FAKE, FAKE, None, FAKE, 1 << 30, None) == -1
+    assert f(FAKE, 10, None, 5, FAKE, 64, 100, None, -1, FAKE, FAKE, None, FAKE, 16, None) == -4
+    assert f(FAKE, 10, None, 0, FAKE, 64, 100, None, -1, None, None, None, None, 0, None) == 0

@@ -100,7 +100,7 @@ def test_attention_canaries(case, step_cache):
         assert torch.equal(x, y), "two runs differ"
 
 
-def _lm_case(H, W, ridx, sup, eos):
+def _lm_case(H, W, ridx, sup, eos, Wp=None):
     import paper_2606_08411_amd as al
     N = ridx.shape[0]
     conf = Guarded(N, torch.float32, 0xFF)
@@ -108,8 +108,12 @@ def _lm_case(H, W, ridx, sup, eos):
     lse = Guarded(N, torch.float32, 0xFF)
     need = al.lmhead_confidence_workspace_size(N, H.shape[1], W.shape[0])
     ws = Guarded(max(need, 16), torch.uint8, 0xFF)
-    al.lmhead_confidence(H, W, row_idx=ridx, suppress_eos=sup, eos_id=eos, conf=conf.view(),
-                         argmax=arg.view(), lse=lse.view(), workspace=ws.view())
+    outs = dict(row_idx=ridx, suppress_eos=sup, eos_id=eos, conf=conf.view(), argmax=arg.view(),
+                lse=lse.view(), workspace=ws.view())
+    if Wp is None:
+        al.lmhead_confidence(H, W, **outs)
+    else:
+        al.lmhead_confidence_packed(H, Wp, W.shape[0], **outs)
     torch.cuda.synchronize()
     assert all(b.guard_ok() for b in (conf, arg, lse, ws)), "a guard band was written"
     assert not torch.isnan(conf.view()).any() and not torch.isnan(lse.view()).any()
@@ -136,6 +140,17 @@ def test_lmhead_canaries(case, step_cache):
     b = _lm_case(H, W, ridx, sup, eos)
     for x, y in zip(a, b):
         assert torch.equal(x, y), "two runs differ"
+    # the packed weight: its copy written into a guarded buffer, then the call
+    import paper_2606_08411_amd as al
+    wp = Guarded(al.lmhead_packed_weight_size(W.shape[1], W.shape[0]) // 2, torch.bfloat16, 0xFF)
+    al.lmhead_pack_weight(W, out=wp.view())
+    torch.cuda.synchronize()
+    assert wp.guard_ok(), "the packed copy overran its buffer"
+    assert not torch.isnan(wp.view().float()).any(), "part of the packed copy was left unwritten"
+    a = _lm_case(H, W, ridx, sup, eos, Wp=wp.view())
+    b = _lm_case(H, W, ridx, sup, eos, Wp=wp.view())
+    for x, y in zip(a, b):
+        assert torch.equal(x, y), "two runs differ (packed)"
 
 
 def _sel_case(s, conf, arg, L, B, row_pos, tokens, masked):

@@ -1,7 +1,8 @@
 """The transfer rule end to end (paper Section 3.2, "Lane-local denoising":
 confidence-based transfer inside each lane's valid update region, refine
-lanes without EOS): GPU lmhead_confidence -> GPU select_unmask against the
-fp64 oracle LM head -> oracle selection, on every workload at seeds 0, 1, 2.
+lanes without EOS): GPU lmhead_confidence (on the plain and on the packed
+weight) -> GPU select_unmask against the fp64 oracle LM head -> oracle
+selection, on every workload at seeds 0, 1, 2.
 
 Several answers are correct where the fp64 and the fp32 computations may
 order two values differently.  Working in the log domain (logconf = m -
@@ -38,10 +39,16 @@ TOL_LSE = 2e-3
 
 
 
-def _gpu_lm(step, W_dev):
+def _gpu_lm(step, W_dev, packed):
+    """The LM head on the plain weight, or on its packed copy."""
     import paper_2606_08411_amd as al
-    conf, arg, lse = al.lmhead_confidence(dev_bf16(step.hidden), W_dev, row_idx=dev(step.row_pos),
-                                          suppress_eos=dev(step.suppress_eos), eos_id=step.eos_id)
+    args = dict(row_idx=dev(step.row_pos), suppress_eos=dev(step.suppress_eos), eos_id=step.eos_id)
+    if packed:
+        Wp = al.lmhead_pack_weight(W_dev)
+        conf, arg, lse = al.lmhead_confidence_packed(dev_bf16(step.hidden), Wp, step.V, **args)
+        del Wp
+    else:
+        conf, arg, lse = al.lmhead_confidence(dev_bf16(step.hidden), W_dev, **args)
     torch.cuda.synchronize()
     return conf, arg, lse
 
@@ -142,21 +149,28 @@ def _run_case(step, W_dev, gpu_lm, ref_lm, mode, fb, k_lane, b_len, tau_future, 
 def test_transfer_rule_chain(name, seed, step_cache, report):
     step = step_cache(name, seed)
     W_dev = dev_bf16(step.W)
-    conf, arg, lse = _gpu_lm(step, W_dev)
     ref_lm = _oracle_lm(step)
+    for packed in (False, True):
+        _chain(step, W_dev, ref_lm, packed, f"{name} seed {seed} {'packed' if packed else 'plain'} W",
+               report)
+
+
+def _chain(step, W_dev, ref_lm, packed, tag, report):
+    conf, arg, lse = _gpu_lm(step, W_dev, packed)
     c, a, ls = conf.cpu().numpy(), arg.cpu().numpy(), lse.cpu().numpy()
     ok = ref_lm["gap"] >= BAND
     n_gap = int((~ok).sum())
     dlog = np.abs((np.log(c.astype(np.float64)) - ref_lm["logconf"])).max()
-    report(f"[{name} seed {seed}] N={step.N} (i) rows with top-2 gap < {BAND}: {n_gap}; "
-          f"max|dconf|={np.abs(c - ref_lm['conf']).max():.2e} max|dlse|="
-          f"{np.abs(ls - ref_lm['lse']).max():.2e} max|dlogconf|={dlog:.2e}")
+    report(f"[{tag}] N={step.N} (i) rows with top-2 gap < {BAND}: {n_gap}; "
+           f"max|dconf|={np.abs(c - ref_lm['conf']).max():.2e} max|dlse|="
+           f"{np.abs(ls - ref_lm['lse']).max():.2e} max|dlogconf|={dlog:.2e}")
     assert np.abs(c - ref_lm["conf"]).max() < TOL_CONF
     assert np.abs(ls - ref_lm["lse"]).max() < TOL_LSE
     assert dlog < BAND / 4            # the exclusion band covers the fp32 error
     assert np.array_equal(a[ok], ref_lm["argmax"][ok])
     assert n_gap <= max(2, step.N // 50)
     gpu_lm = (conf, arg, lse)
+    seed = step.seed
     rng = np.random.default_rng([seed, 31])
     k_lane = rng.integers(0, step.B + 1, step.L).astype(np.int32)
     b_win = rng.integers(step.B // 2, step.B + 1, step.L).astype(np.int32)
@@ -170,7 +184,7 @@ def test_transfer_rule_chain(name, seed, step_cache, report):
     excluded = 0
     for mode, fb, kl, bl, tf in cases:
         excluded += _run_case(step, W_dev, gpu_lm, ref_lm, mode, fb, kl, bl, tf,
-                              f"{name} seed {seed} mode {mode} fb {fb} tf {tf}", report)
+                              f"{tag} mode {mode} fb {fb} tf {tf}", report)
     # Near-ties are rare on these inputs; a flood of exclusions would mean the
     # comparison checks nothing.
     assert excluded <= max(1, len(cases) * step.L // 8)

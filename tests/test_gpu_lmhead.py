@@ -121,3 +121,75 @@ def test_lmhead_repeatable(step_cache):
     b = _run(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+# ------------------------------------------------------------- packed weight
+def _packed_reference(W):
+    """The packed layout written out from its definition in the header:
+    32-row units u, 64-element K chunks c; block (c, u) holds step s, lane
+    l = 32 h + r, element e = row 32u + r, K index 64c + 16s + 8h + e;
+    blocks K-chunk major; zero padding."""
+    V, d = W.shape
+    U, C = -(-V // 32), -(-d // 64)
+    Wp = np.zeros((U * 32, C * 64), np.uint16)
+    Wp[:V, :d] = W
+    out = np.empty((C, U, 4, 64, 8), np.uint16)
+    for c in range(C):
+        for u in range(U):
+            for s in range(4):
+                for h in range(2):
+                    out[c, u, s, 32 * h:32 * h + 32, :] = \
+                        Wp[32 * u:32 * u + 32, 64 * c + 16 * s + 8 * h:64 * c + 16 * s + 8 * h + 8]
+    return out.reshape(-1)
+
+
+@pytest.mark.parametrize("V,d", [(64, 64), (1000, 200), (4097, 136), (33, 8)])
+def test_lmhead_pack_layout(V, d):
+    import paper_2606_08411_amd as al
+    g = np.random.default_rng([V, d])
+    W = g.integers(0, 1 << 16, (V, d)).astype(np.uint16)
+    got = al.lmhead_pack_weight(dev_bf16(W))
+    torch.cuda.synchronize()
+    assert got.numel() * 2 == al.lmhead_packed_weight_size(d, V)
+    assert np.array_equal(got.view(torch.int16).cpu().numpy().view(np.uint16), _packed_reference(W))
+
+
+def _run_packed(hidden_bits, W_bits, row_idx, sup, eos_id):
+    import paper_2606_08411_amd as al
+    Wp = al.lmhead_pack_weight(dev_bf16(W_bits))
+    conf, arg, lse = al.lmhead_confidence_packed(
+        dev_bf16(hidden_bits), Wp, W_bits.shape[0],
+        row_idx=None if row_idx is None else dev(row_idx),
+        suppress_eos=None if sup is None else dev(sup), eos_id=eos_id)
+    torch.cuda.synchronize()
+    return conf.cpu().numpy(), arg.cpu().numpy(), lse.cpu().numpy()
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=[str(c) for c in SWEEP])
+def test_lmhead_packed_sweep(case):
+    """The packed path against the oracle on every kernel variant of the
+    sweep.  (It tiles the vocabulary in 32-row units, the plain path in
+    rows, so the two group their fp32 sums differently and agree only to
+    rounding.)"""
+    N, n_rows, d, V, eos = case
+    g = np.random.default_rng([N, d, V])
+    scale = g.uniform(1, 6, n_rows).astype(np.float32)
+    H = synth.f32_to_bf16_bits(g.standard_normal((n_rows, d), dtype=np.float32) * scale[:, None])
+    W = synth.f32_to_bf16_bits(g.standard_normal((V, d), dtype=np.float32) / np.float32(np.sqrt(d)))
+    row_idx = np.sort(g.choice(n_rows, N, replace=False)).astype(np.int32)[::-1].copy()
+    sup = (g.random(N) < 0.5).astype(np.uint8)
+    gpu = _run_packed(H, W, row_idx, sup, eos)
+    ref = oracle.lmhead.lmhead_confidence_full(f32(H), row_idx, f32(W), sup, eos)
+    _compare(gpu, ref, "packed " + str(case))
+
+
+@pytest.mark.parametrize("name", ["llada", "dream", "wide"])
+def test_lmhead_packed_workloads(name, step_cache):
+    step = step_cache(name, 0)
+    gpu = _run_packed(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
+    sample = np.arange(step.N)
+    if step.N > 128:
+        sample = np.sort(np.random.default_rng([0, 78]).choice(step.N, 48, replace=False))
+    ref = oracle.lmhead.lmhead_confidence_full(
+        f32(step.hidden), step.row_pos[sample], f32(step.W), step.suppress_eos[sample], step.eos_id)
+    _compare(tuple(x[sample] for x in gpu), ref, "packed " + name)
