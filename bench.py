@@ -249,6 +249,7 @@ def decode_bench(args):
     W = torch.from_numpy(np.ascontiguousarray(s.W).view(np.int16)).view(torch.bfloat16).to(dev)
     W[0:2] *= 2.5
     W[2] *= 1.8
+    W_packed = al.lmhead_pack_weight(W) if args.w_layout == "packed" else None
     H = bf(rng.standard_normal((4 * L, s.d)) * rng.uniform(1, 6, (4 * L, 1)))
     pool = lambda n, h: bf(rng.standard_normal((n, h, s.D)))
     q, kl, vl = pool(64 * Wb, s.Hq), pool(64 * Wb, s.Hkv), pool(64 * Wb, s.Hkv)
@@ -314,9 +315,14 @@ def decode_bench(args):
             tok_d = up_d[o_tok:o_tok + 4 * nb].view(torch.int32)
             sup = up_d[o_sup:o_sup + nr]
             msk_d = up_d[o_msk:o_msk + nb]
-            conf, arg, _ = al.lmhead_confidence(H, W, row_idx=row_idx, suppress_eos=sup,
-                                                eos_id=s.eos_id, conf=conf_d, argmax=arg_d,
-                                                want_lse=False)
+            if W_packed is not None:
+                conf, arg, _ = al.lmhead_confidence_packed(H, W_packed, s.V, row_idx=row_idx,
+                                                           suppress_eos=sup, eos_id=s.eos_id,
+                                                           conf=conf_d, argmax=arg_d, want_lse=False)
+            else:
+                conf, arg, _ = al.lmhead_confidence(H, W, row_idx=row_idx, suppress_eos=sup,
+                                                    eos_id=s.eos_id, conf=conf_d, argmax=arg_d,
+                                                    want_lse=False)
             al.select_unmask(conf, arg, rows_d, tok_d, msk_d, n, Wb,
                              pl["role"], pl["b_len"], pl["t_step"], al.MODE_THRESHOLD, s.tau,
                              1, None, s.delim_ids, s.eos_id, s.rho_min, s.t_min,
@@ -345,7 +351,8 @@ def decode_bench(args):
         "value": round(n_out / dt, 1), "unit": "tokens/s", "n_gpus": 1,
         "higher_is_better": True, "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[args.config] + f"; decode of {L} positions, block "
-                   f"{B}, lookahead window {window}, delimiter rows of W x2.5, EOS row x1.8",
+                   f"{B}, lookahead window {window}, delimiter rows of W x2.5, EOS row x1.8, "
+                   f"{args.w_layout} LM-head weight",
                    "name": args.config, "seed": args.seed, "L_gen": L, "B": B, "window": window},
         "ms_per_decode": round(dt * 1000, 3), "runs": args.decode_runs,
         "iterations": c["iterations"], "nfe": c["nfe"], "forks": c["forks"],

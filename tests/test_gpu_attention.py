@@ -93,6 +93,16 @@ def test_attention_workloads(name, seed, step_cache):
         assert np.abs(out["lse_ref"][rr] - l_r).max() < TOL_LSE
 
 
+@pytest.mark.parametrize("name", ["llada", "dream", "long", "wide"])
+def test_attention_workloads_every_element(name, step_cache):
+    """Every output element at full size (seed 0): all lane rows and heads
+    against oracle form A, and at Wide every refresh row and the rewritten
+    prefix."""
+    step = step_cache(name, 0, with_weight=False)
+    out = _run(step)
+    _check_full(step, out)
+
+
 SWEEP = [
     # D, B, L, tree, Hq, Hkv, P, refresh_frac
     (64, 16, 1, "linear", 2, 2, 0, 0.0),

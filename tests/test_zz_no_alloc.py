@@ -61,3 +61,33 @@ def test_noalloc_matches_workspace_entry():
         for a, b, name in zip(got, want, ("conf", "argmax", "lse")):
             assert torch.equal(a, b), f"call {k} ({N} rows): {name} differs"
         assert not torch.isnan(got[0]).any() and (got[1] >= 0).all()
+
+
+def test_noalloc_in_graph_capture():
+    """The use it exists for: captured into a HIP graph (no allocation
+    during capture), replayed several times with eager work of another
+    shape in between; every replay equals the eager call."""
+    import paper_2606_08411_amd as al
+    H, W, ridx, sup = _inputs(200, 256, 512, 40000, seed=3)
+    H2, W2, ridx2, sup2 = _inputs(50, 64, 256, 9000, seed=4)
+    want = _outputs(200)
+    al.lmhead_confidence_noalloc(H, W, row_idx=ridx, suppress_eos=sup, eos_id=2, conf=want[0],
+                                 argmax=want[1], lse=want[2])
+    got = _outputs(200)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        al.lmhead_confidence_noalloc(H, W, row_idx=ridx, suppress_eos=sup, eos_id=2, conf=got[0],
+                                     argmax=got[1], lse=got[2])
+    torch.cuda.synchronize()
+    other = _outputs(50)
+    for rep in range(3):
+        for t in got:
+            t.fill_(0)
+        al.lmhead_confidence_noalloc(H2, W2, row_idx=ridx2, suppress_eos=sup2, eos_id=1,
+                                     conf=other[0], argmax=other[1], lse=other[2])
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b, name in zip(got, want, ("conf", "argmax", "lse")):
+            assert torch.equal(a, b), f"replay {rep}: {name} differs from the eager call"
