@@ -427,11 +427,24 @@ constexpr int lm_rt(int nf) { return nf <= 3 ? 2 : 1; }
 constexpr int lm_pf(int nf) { return nf <= 3 ? 1 : (nf == 4 ? 3 : 2); }
 constexpr int lm_sc(int nf) { return nf <= 4 ? 4 : 2; }
 constexpr int LM_KC = 64;
-constexpr int lm_vt(int nf) { return 32 * lm_rt(nf) * LM_WAVES; }
+// More than 224 columns take several column tiles, each streaming W
+// again (mostly from L2: the column tiles of a vocab tile run on
+// neighbouring workgroups).  On the packed weight, 128-column tiles with
+// two 32-row tiles per wavefront replace 224-column tiles with one there:
+// every B fragment read from LDS feeds two MFMAs, which is what bounds
+// these shapes (LDS reads of the hidden rows, not HBM).  Wide shape, N =
+// 614 (one box, two runs each): 710 us against 776 us per call; at 128
+// and 205 columns (one column tile) the same change is slower (Dream +8%,
+// Long +2.5%), and on the plain weight too (801 against 735 us: that
+// variant spills).
+constexpr int LM_MULTI_NF = 4;
+constexpr int LM_MULTI_PF = 1;
+constexpr int LM_MULTI_SC = 2;
 
-// Column tiling: n_nt tiles of nf 32-column fragments (<= 224 columns).
+// Column tiling: n_nt tiles of nf 32-column fragments (<= 224 columns),
+// rt 32-row vocabulary tiles per wavefront.
 struct LmLayout {
-  int nf, nt_cols, n_nt, n_vt;
+  int nf, rt, nt_cols, n_nt, n_vt;
   size_t total;
 };
 
@@ -454,15 +467,18 @@ static int lm_cu_count() {
 static LmLayout lm_layout(int N, int V, bool packed) {
   LmLayout L{};
   const int frags = N > 0 ? (N + 31) / 32 : 1;
-  L.n_nt = N > 0 ? (frags + LM_MAX_NF - 1) / LM_MAX_NF : 0;
+  const bool multi = packed && frags > LM_MAX_NF;
+  const int per_tile = multi ? LM_MULTI_NF : LM_MAX_NF;
+  L.n_nt = N > 0 ? (frags + per_tile - 1) / per_tile : 0;
   L.nf = N > 0 ? (frags + L.n_nt - 1) / L.n_nt : 1;
+  L.rt = multi ? 2 : lm_rt(L.nf);
   L.nt_cols = 32 * L.nf;
   // One workgroup per CU runs at a time.  When the vocabulary needs more
   // than one round of full tiles, the tile count is rounded up to a
   // multiple of the CU count and the rows are spread evenly, so the last
   // round is not partly empty (V = 152064: 594 full tiles would take 3
   // rounds at 77% use; 768 tiles of 198 rows take 3 even rounds).
-  const int vt_rows = lm_vt(L.nf);
+  const int vt_rows = 32 * L.rt * LM_WAVES;
   const int base = packed ? ((V + 31) / 32 + vt_rows / 32 - 1) / (vt_rows / 32)
                           : (V + vt_rows - 1) / vt_rows;
   const int units = lm_cu_count();
@@ -576,7 +592,16 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
       if (packed) AL_LM_LAUNCH(F, false, true); else AL_LM_LAUNCH(F, false, false);           \
     }                                                                                         \
     break;
-  switch (L.nf) {
+#define AL_LM_MULTI(RG, PK)                                                                   \
+  hipLaunchKernelGGL((lmhead_partial_kernel<LM_MULTI_NF, RG, LM_WAVES, LM_KC, LM_MULTI_PF, 2,  \
+                                            LM_MULTI_SC, false, PK>),                         \
+                     grid, block, 0, stream, p)
+  if (L.nf == LM_MULTI_NF && L.rt == 2) {  // only the packed layout tiles this way
+    if (d % (LM_KC * LM_MULTI_SC) != 0)
+      AL_LM_MULTI(true, true);
+    else
+      AL_LM_MULTI(false, true);
+  } else switch (L.nf) {
     AL_LM_CASE(1)
     AL_LM_CASE(2)
     AL_LM_CASE(3)
@@ -587,6 +612,7 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
       AL_LM_CASE(7)
   }
 #undef AL_LM_CASE
+#undef AL_LM_MULTI
 #undef AL_LM_LAUNCH
   hipLaunchKernelGGL(lmhead_merge_kernel, dim3(N), dim3(LM_MERGE_THREADS), 0, stream, p.part, N,
                      L.n_vt, L.nt_cols, conf, argmax, lse);

@@ -67,6 +67,9 @@ SWEEP = [  # N, n_rows, d, V, eos
     (420, 450, 96, 700, 9), (225, 225, 64, 300, 1), (40, 40, 16, 70000, 3),
     (128, 130, 40, 900, 7), (100, 110, 448, 2000, 1), (120, 120, 328, 1200, 0),
     (97, 100, 64, 70000, 3),
+    # more than 224 columns: 128-column tiles with two row tiles per
+    # wavefront, d a multiple of 128 (plain variant) and 96-column tiles
+    (500, 520, 256, 3001, 4), (270, 300, 128, 2000, 5),
 ]
 
 
