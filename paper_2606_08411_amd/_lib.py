@@ -314,16 +314,24 @@ def lmhead_confidence_workspace_size(N, d, V) -> int:
     return int(library().lmhead_confidence_workspace_size(N, d, V))
 
 
-def _lmhead_args(hidden, W, row_idx, suppress_eos, conf, argmax, lse, want_lse):
-    """Checks and output allocation shared by the two LM-head calls."""
+def _lmhead_args(hidden, W, row_idx, suppress_eos, conf, argmax, lse, want_lse, V=None):
+    """Checks and output allocation shared by the LM-head calls.  W is the
+    [V][d] weight, or (V given) the flat packed copy of a [V][d] weight."""
     bf16 = torch.bfloat16
     _tensor(hidden, "hidden", bf16)
     if hidden.dim() != 2:
         raise AsyncLaneError(f"hidden: [n_rows][d] expected, got shape {tuple(hidden.shape)}")
     n_rows, d = hidden.shape
-    _tensor(W, "W", bf16)
-    if W.dim() != 2 or W.shape[1] != d:
-        raise AsyncLaneError(f"W: [V][d={d}] expected, got shape {tuple(W.shape)}")
+    if V is None:
+        _tensor(W, "W", bf16)
+        if W.dim() != 2 or W.shape[1] != d:
+            raise AsyncLaneError(f"W: [V][d={d}] expected, got shape {tuple(W.shape)}")
+        V = int(W.shape[0])
+    else:
+        nbytes = int(library().lmhead_packed_weight_size(int(d), int(V)))
+        if nbytes == 0:
+            raise AsyncLaneError(f"W_packed: no packed layout for d={d}, V={V}")
+        _tensor(W, "W_packed", bf16, min_numel=nbytes // 2)
     N = n_rows
     if row_idx is not None:
         _tensor(row_idx, "row_idx", torch.int32)
@@ -342,7 +350,7 @@ def _lmhead_args(hidden, W, row_idx, suppress_eos, conf, argmax, lse, want_lse):
     _tensor(argmax, "argmax", torch.int32, min_numel=N)
     _tensor(lse, "lse", torch.float32, min_numel=N, optional=True)
     _same_device(hidden, W, row_idx, suppress_eos, conf, argmax, lse)
-    return n_rows, d, int(W.shape[0]), N, conf, argmax, lse
+    return n_rows, d, int(V), N, conf, argmax, lse
 
 
 def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
@@ -402,17 +410,8 @@ def lmhead_confidence_packed(hidden, W_packed, V, row_idx=None, suppress_eos=Non
     """lmhead_confidence reading the weight from lmhead_pack_weight's copy
     (V = vocabulary size of the original W; d is hidden's width)."""
     lib = library()
-    _tensor(hidden, "hidden", torch.bfloat16)
-    if hidden.dim() != 2:
-        raise AsyncLaneError(f"hidden: [n_rows][d] expected, got shape {tuple(hidden.shape)}")
-    d = int(hidden.shape[1])
-    V = int(V)
-    nbytes = int(lib.lmhead_packed_weight_size(d, V))
-    _tensor(W_packed, "W_packed", torch.bfloat16, min_numel=max(nbytes // 2, 1))
-    # the shared checks see W_packed as a [1][d] weight (its dtype and device)
-    n_rows, d, _, N, conf, argmax, lse = _lmhead_args(hidden, W_packed.view(-1)[:d].view(1, d),
-                                                      row_idx, suppress_eos, conf, argmax, lse,
-                                                      want_lse)
+    n_rows, d, V, N, conf, argmax, lse = _lmhead_args(hidden, W_packed, row_idx, suppress_eos, conf,
+                                                      argmax, lse, want_lse, V=int(V))
     if N == 0:
         return conf, argmax, lse
     dev = hidden.device

@@ -126,3 +126,18 @@ def test_select_out_buffers_checked():
     out["unmasked_pos"] = torch.zeros(5, dtype=torch.int32)
     with pytest.raises(AsyncLaneError, match="missing 'counts'"):
         al.select_unmask(**_sel_args(), out=out)
+
+
+def test_lmhead_packed_rejects():
+    a = _lm_args()
+    Wp = torch.zeros(al.lmhead_packed_weight_size(64, 100) // 2, dtype=bf16)
+    with pytest.raises(AsyncLaneError, match="W_packed:"):
+        al.lmhead_confidence_packed(a["hidden"], Wp[:-1], 100, row_idx=a["row_idx"])
+    with pytest.raises(AsyncLaneError, match="W_packed: dtype"):
+        al.lmhead_confidence_packed(a["hidden"], Wp.float(), 100, row_idx=a["row_idx"])
+    with pytest.raises(AsyncLaneError, match="W_packed: no packed layout"):
+        al.lmhead_confidence_packed(torch.zeros(8, 12, dtype=bf16), Wp, 100)
+    with pytest.raises(AsyncLaneError, match="device tensor expected"):
+        al.lmhead_confidence_packed(a["hidden"], Wp, 100, row_idx=a["row_idx"])
+    with pytest.raises(AsyncLaneError, match="W: dtype"):
+        al.lmhead_pack_weight(torch.zeros(100, 64))
