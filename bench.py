@@ -13,6 +13,7 @@ cpu_baseline the fp64 oracle on a bounded sample of the same workload,
 """
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -84,11 +85,21 @@ def lmhead_bytes(s):
     return 2.0 * s.V * s.d + 2.0 * s.N * s.d + 12.0 * s.N
 
 
+def _code_only(text):
+    """C++ source without comments, trailing blanks and empty lines (the
+    kernel sources hold no string literal containing a comment marker)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+
+
 def kernel_source_hash():
+    """Hash of the LM-head kernel code (comments excluded, so counters stay
+    attached to the code they were taken on when only comments change)."""
     h = hashlib.sha256()
     for f in ("lmhead.hip", "common.h"):
-        with open(os.path.join(ROOT, "paper_2606_08411_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2606_08411_amd", "csrc", f)) as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

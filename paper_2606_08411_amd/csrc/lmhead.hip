@@ -431,12 +431,12 @@ constexpr int LM_KC = 64;
 // again (mostly from L2: the column tiles of a vocab tile run on
 // neighbouring workgroups).  On the packed weight, 128-column tiles with
 // two 32-row tiles per wavefront replace 224-column tiles with one there:
-// every B fragment read from LDS feeds two MFMAs, which is what bounds
-// these shapes (LDS reads of the hidden rows, not HBM).  Wide shape, N =
-// 614 (one box, two runs each): 710 us against 776 us per call; at 128
-// and 205 columns (one column tile) the same change is slower (Dream +8%,
-// Long +2.5%), and on the plain weight too (801 against 735 us: that
-// variant spills).
+// every B fragment read from LDS feeds two MFMAs, and a workgroup's
+// hidden block serves 512 vocab rows instead of 256 (these shapes are not
+// HBM-bound).  Wide shape, N = 614 (one box, two runs each): 710 us
+// against 776 us per call; at 128 and 205 columns (one column tile) the
+// same change is slower (Dream +8%, Long +2.5%), and on the plain weight
+// too (801 against 735 us: that variant spills).
 constexpr int LM_MULTI_NF = 4;
 constexpr int LM_MULTI_PF = 1;
 constexpr int LM_MULTI_SC = 2;
