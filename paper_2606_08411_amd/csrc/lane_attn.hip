@@ -6,7 +6,7 @@
 // rows see the shared cached prefix, the blocks of its ancestors in the lane
 // tree and, bidirectionally, its own block.
 //
-// Kernel layout.  A workgroup of 4 wavefronts serves one K/V head and four
+// Kernel layout.  A workgroup of 8 wavefronts serves one K/V head and eight
 // query tiles (32 query rows of one lane and one query head each; for
 // grouped-query attention the Hq/Hkv heads of a lane are adjacent tiles).
 // Key tiles of 64 rows are staged once per workgroup in LDS, K and V both
@@ -35,7 +35,7 @@
 
 namespace al {
 
-constexpr int AT_WAVES = 4;
+constexpr int AT_WAVES = 8;
 constexpr int AT_THREADS = AT_WAVES * kWave;
 constexpr int AT_KT = 64;  // keys per staged tile
 constexpr int AT_MAX_LANES = 64;
@@ -58,11 +58,15 @@ struct AttnParams {
   unsigned long long vis[AT_MAX_LANES];  // bit j: lane block j visible to lane i
 };
 
-// Two wavefronts per SIMD (<= 256 registers each, no spills at D = 128):
-// with two workgroups per CU, one workgroup's tile staging (loads, the
-// transposed V store, barriers) overlaps the other's MFMAs.  At one
-// wavefront per SIMD (312 registers) the phases serialize: 530 us vs
-// 270 us on the Wide lane pass (MI355X).
+// Two wavefronts per SIMD (<= 256 registers each, no spills at D = 128),
+// one workgroup per CU: the next tile's loads go to registers while the
+// current tile is multiplied, and the two wavefronts of a SIMD interleave
+// their MFMA and VALU phases.  At one wavefront per SIMD (312 registers)
+// the phases serialize: 530 us vs 270 us on the Wide lane pass (MI355X).
+// Eight query tiles per workgroup instead of four (two 4-wavefront
+// workgroups per CU) halve the K/V staging per MFMA: Wide lane + refresh
+// passes 293-297 us against 308-310 us per call, Long 53 us either way
+// (one box, two runs each; identical outputs).
 constexpr int AT_OCC = 2;
 
 template <int D>
@@ -693,15 +697,16 @@ __global__ __launch_bounds__(256) void prefix_scatter_kernel(const int32_t* idx,
 
 // ------------------------------------------------------------------ host
 static int choose_split(int base_wgs, int total_key_tiles) {
-  // Short grids on the 4-tile kernel leave CUs idle: split the key tiles
-  // until about 512 workgroups exist (two per CU at two wavefronts per
+  // Short grids on the 8-tile kernel leave CUs idle: split the key tiles
+  // until about 256 workgroups exist (one per CU at two wavefronts per
   // SIMD), keeping at least 3 key tiles per split, since each split adds
-  // partials to merge.  Measured with the merge (MI355X, best in [1, 16]):
+  // partials to merge.  Measured with the merge on 4-wavefront workgroups
+  // (MI355X, best in [1, 16]):
   // Long 4 splits, 62.8 us (128 us unsplit); Wide 1, 277 us (the LLaDA and
   // Dream step shapes, 4 and 8 splits here, now take the wavefront-split
   // kernel).
   int s = 1;
-  while (s < 16 && base_wgs * s < 512 && total_key_tiles >= 3 * (2 * s)) s *= 2;
+  while (s < 16 && base_wgs * s < 256 && total_key_tiles >= 3 * (2 * s)) s *= 2;
   return s;
 }
 
@@ -725,7 +730,7 @@ static PassShape pass_shape(int n_rows, int rows_per_lane, int n_lanes, int g, i
 
 // The wavefront-split kernel when its grid fits the chip in one round (one
 // workgroup per CU: 256 on MI355X) and no wavefront takes more than 8 key
-// units; otherwise the 4-query-tile kernel, whose shared K/V staging wins
+// units; otherwise the 8-query-tile kernel, whose shared K/V staging wins
 // on large grids and long key ranges.  Measured per call after a
 // cache-evicting copy (MI355X): LLaDA step shape 16.6 us against 19.7 us,
 // Dream 20.9 against 30.0; Long 56.6 against 57.0 (512 workgroups: stays),
