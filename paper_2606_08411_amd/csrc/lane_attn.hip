@@ -214,6 +214,13 @@ void lane_attn_kernel(AttnParams p) {
   // One staged tile: S^T = K Q^T, the online softmax update in log2 units,
   // then O^T += V^T P^T.  Only ragged tiles (nvalid < 64) mask; a 32-key
   // half with no valid key is skipped in both products.
+  //
+  // Wavefront priority: low for the two MFMA blocks, high for the softmax
+  // and for the tile staging between tiles, so the SIMD's arbiter favours
+  // the wavefront whose vector work the next MFMAs wait for while the other
+  // wavefront's MFMAs run (graph replay, one box, two runs each: Wide lane
+  // + refresh 253-254 us against 259-260 us, Long 50-51 us against 52-53;
+  // no gain on the wavefront-split kernel's shapes).
   auto tile_compute = [&](int nvalid) {
     const int nsub = (nvalid + 31) >> 5;  // 32-key halves holding valid keys
     const f32x16 zero16 = {};
@@ -221,6 +228,7 @@ void lane_attn_kernel(AttnParams p) {
     auto kfrag = [&](int kb, int ks) {
       return *reinterpret_cast<const bf16x8*>(&k_s[(kb * 32 + r32) * KSTR + ks * 16 + hh * 8]);
     };
+    __builtin_amdgcn_s_setprio(0);
     if (nsub == 2) {
       // Both 32-key halves: the two accumulation chains interleave, so
       // consecutive MFMAs are independent.
@@ -248,6 +256,7 @@ void lane_attn_kernel(AttnParams p) {
           sacc[kb][r] = (key < nvalid) ? sacc[kb][r] : -INFINITY;
         }
     }
+    __builtin_amdgcn_s_setprio(1);
     // The max is taken on the raw scores (the scale is positive, so
     // max-then-scale is exact); each exponent is then one FMA.
     float mx = -INFINITY;
@@ -287,6 +296,7 @@ void lane_attn_kernel(AttnParams p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
     }
+    __builtin_amdgcn_s_setprio(0);
     // O^T += V^T P^T, one 16-key MFMA step at a time.  The V^T fragment
     // of lane (d, h) is keys 16 ks2 + 4h + {0..3, 8..11} at column d: two
     // transpose reads of 4 x 16 blocks of the row-major V tile.
@@ -301,6 +311,7 @@ void lane_attn_kernel(AttnParams p) {
         }
       }
     }
+    __builtin_amdgcn_s_setprio(1);
   };
 
   int kt = kt0;
