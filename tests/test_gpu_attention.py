@@ -118,10 +118,10 @@ SWEEP = [
     (64, 1024, 2, "fork", 16, 1, 64, 0.0),      # largest block, largest GQA group
     (128, 32, 64, "forest", 4, 1, 0, 0.0),      # no prefix, 64 roots: 256 workgroups of
                                                 # the wavefront-split kernel, 64 units
-    (128, 32, 64, "forest", 8, 2, 0, 0.0),      # the same on the 4-tile kernel: many key
+    (128, 32, 64, "forest", 8, 2, 0, 0.0),      # the same on the 8-tile kernel: many key
                                                 # splits hold no tile any wavefront of a
                                                 # workgroup sees (empty-split path)
-    (128, 48, 12, "random", 16, 2, 333, 0.2),   # 4-tile kernel (384 query tiles) with
+    (128, 48, 12, "random", 16, 2, 333, 0.2),   # 8-tile kernel (384 query tiles) with
                                                 # 2 row tiles per lane; refresh rows on
                                                 # the wavefront-split kernel
     (128, 16, 40, "random", 4, 2, 700, 0.0),    # wavefront-split kernel at its unit
@@ -141,11 +141,11 @@ def test_attention_sweep(case):
 def _random_cases(n=10, seed=2606):
     """Seeded random valid shapes on both sides of the kernel choice (at
     most 256 query tiles x heads and 64 32-key units per tile take the
-    wavefront-split kernel, larger ones the 4-tile kernel)."""
+    wavefront-split kernel, larger ones the 8-tile kernel)."""
     rng = np.random.default_rng(seed)
     cases = []
     for k in range(n):
-        big = k % 2 == 1          # long prefix or many heads: the 4-tile kernel
+        big = k % 2 == 1          # long prefix or many heads: the 8-tile kernel
         Hkv = int(rng.choice([4, 8] if big else [1, 2, 4]))
         g = int(rng.choice([2, 4] if big else [1, 2, 4, 7]))
         L = int(rng.integers(6, 11) if big else rng.integers(1, 13))

@@ -4,7 +4,7 @@ Rules: argmax must match bit-exactly except on rows whose oracle top-2
 logits differ by less than 1e-3 (several answers are then correct; those
 rows are counted and reported, and must be rare); conf within 2e-2 max abs
 (expected ~1e-5); lse within 2e-3.  Full-size workloads score every masked
-row (LLaDA, Dream) or a seeded sample of rows (Long, Wide).
+row (also at seeds 1 and 2 through the chain test).
 """
 import numpy as np
 import pytest
@@ -45,12 +45,9 @@ def _compare(gpu, ref, label):
 def test_lmhead_workloads(name, step_cache):
     step = step_cache(name, 0)
     gpu = _run(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
-    sample = np.arange(step.N)
-    if step.N > 128:
-        sample = np.sort(np.random.default_rng([0, 77]).choice(step.N, 48, replace=False))
     ref = oracle.lmhead.lmhead_confidence_full(
-        f32(step.hidden), step.row_pos[sample], f32(step.W), step.suppress_eos[sample], step.eos_id)
-    _compare(tuple(x[sample] for x in gpu), ref, name)
+        f32(step.hidden), step.row_pos, f32(step.W), step.suppress_eos, step.eos_id)
+    _compare(gpu, ref, name)
 
 
 SWEEP = [  # N, n_rows, d, V, eos
@@ -190,9 +187,6 @@ def test_lmhead_packed_sweep(case):
 def test_lmhead_packed_workloads(name, step_cache):
     step = step_cache(name, 0)
     gpu = _run_packed(step.hidden, step.W, step.row_pos, step.suppress_eos, step.eos_id)
-    sample = np.arange(step.N)
-    if step.N > 128:
-        sample = np.sort(np.random.default_rng([0, 78]).choice(step.N, 48, replace=False))
     ref = oracle.lmhead.lmhead_confidence_full(
-        f32(step.hidden), step.row_pos[sample], f32(step.W), step.suppress_eos[sample], step.eos_id)
-    _compare(tuple(x[sample] for x in gpu), ref, "packed " + name)
+        f32(step.hidden), step.row_pos, f32(step.W), step.suppress_eos, step.eos_id)
+    _compare(gpu, ref, "packed " + name)

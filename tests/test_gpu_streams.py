@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 
 
 def _problem(seed):
-    s = synth.make_step("long", seed, with_weight=False)   # 4-tile kernel with key splits
+    s = synth.make_step("long", seed, with_weight=False)   # shared-staging kernel with key splits
     g = np.random.default_rng([seed, 3])
     N, d, V = 205, 1024, 70000
     H = synth.f32_to_bf16_bits(g.standard_normal((300, d), dtype=np.float32) *
