@@ -476,13 +476,23 @@ static LmLayout lm_layout(int N, int V, bool packed) {
   // One workgroup per CU runs at a time.  When the vocabulary needs more
   // than one round of full tiles, the tile count is rounded up to a
   // multiple of the CU count and the rows are spread evenly, so the last
-  // round is not partly empty (V = 152064: 594 full tiles would take 3
-  // rounds at 77% use; 768 tiles of 198 rows take 3 even rounds).
+  // round is not partly empty (V = 152064 on W as given: 594 full tiles
+  // would take 3 rounds at 77% use; 768 tiles of 198 rows take 3 even
+  // rounds).  A packed tile holds whole 32-row units, one per wavefront
+  // row tile; where the even spread would leave more than 1/8 of those
+  // slots repeating a tile's last unit (MFMA work without new W), the full
+  // tiles are kept: V = 152064 at 128 columns takes 594 tiles of 8 units
+  // instead of 768 of 6.19 (per call, one box, three runs each: 262-272
+  // us against 279-287 us).
   const int vt_rows = 32 * L.rt * LM_WAVES;
   const int base = packed ? ((V + 31) / 32 + vt_rows / 32 - 1) / (vt_rows / 32)
                           : (V + vt_rows - 1) / vt_rows;
   const int units = lm_cu_count();
   L.n_vt = base <= units ? base : units * ((base + units - 1) / units);
+  if (packed && L.n_vt > base) {
+    const long long n_hg = (V + 31) / 32, slots = (long long)L.n_vt * (vt_rows / 32);
+    if (8 * n_hg < 7 * slots) L.n_vt = base;
+  }
   L.total = sizeof(LmPartial) * (size_t)L.n_nt * L.n_vt * L.nt_cols;
   return L;
 }
