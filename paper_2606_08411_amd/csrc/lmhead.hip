@@ -15,10 +15,12 @@
 //   bf16 MFMA) and loads them straight into registers, one to three chunks
 //   ahead; each W element is used by one wavefront only;
 // * the scored hidden rows (B operand, <= 224 rows per column tile; more
-//   rows take several tiles, each streaming W again) are staged per block
-//   of K once per workgroup in LDS and shared by its 8 wavefronts;
+//   rows take several tiles of 224, or of 128 on the packed weight, each
+//   streaming W again) are staged per block of K once per workgroup in LDS
+//   and shared by its 8 wavefronts;
 // * workgroups are dealt to the 8 XCDs in contiguous runs of vocab tiles;
-//   the 512-row workgroups walk K in a rotated order per group of tiles;
+//   on W as given the 512-row workgroups walk K in a rotated order per
+//   group of tiles (the packed copy, read chunk-major, needs none);
 // * the epilogue writes one partial (m, s, argmax) per column and vocab
 //   tile; lmhead_merge_kernel combines them in a fixed order, so results
 //   are bitwise reproducible.  (A single-kernel merge by the last workgroup
