@@ -132,6 +132,18 @@ def _same_device(*ts):
         raise AsyncLaneError(f"tensors on different devices: {sorted(str(d) for d in devs)}")
 
 
+def _call(fn, t, *args):
+    """Call library function fn with t's device current: the ABI takes device
+    pointers (and the stream) of the current HIP device, and the library's
+    per-device state (compute-unit count, the no-alloc array's address) is
+    looked up on the current device."""
+    idx = t.device.index
+    if idx is not None and idx != torch.cuda.current_device():
+        with torch.cuda.device(idx):
+            return fn(*args)
+    return fn(*args)
+
+
 # torch's raw-handle accessor costs ~0.1 us against ~3 us for
 # torch.cuda.current_stream(); both name the same stream.
 _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
@@ -286,7 +298,8 @@ def lane_attn_forward(q, k_lane, v_lane, k_prefix, v_prefix, parent, B, scale=0.
     stream = _stream(k_prefix)
     if workspace is None:
         ws, ws_bytes = _workspace("attn", need, dev, stream)
-    st = lib.lane_attn_forward(
+    st = _call(
+        lib.lane_attn_forward, k_prefix,
         _ptr(q), _ptr(k_lane), _ptr(v_lane), _ptr(k_prefix), _ptr(v_prefix),
         _np_ptr(par) if L else None,
         L, B, P, Hq, Hkv, D, float(scale),
@@ -373,9 +386,10 @@ def lmhead_confidence(hidden, W, row_idx=None, suppress_eos=None, eos_id=-1,
     stream = _stream(hidden)
     if workspace is None:
         ws, ws_bytes = _workspace("lmhead", need, dev, stream)
-    st = lib.lmhead_confidence(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
-                               _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
-                               _ptr(lse), _ptr(ws), ws_bytes, stream)
+    st = _call(lib.lmhead_confidence, hidden,
+               _ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
+               _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
+               _ptr(lse), _ptr(ws), ws_bytes, stream)
     _check(st, "lmhead_confidence")
     return conf, argmax, lse
 
@@ -400,7 +414,7 @@ def lmhead_pack_weight(W, out=None):
         out = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=W.device)
     _tensor(out, "out", torch.bfloat16, min_numel=nbytes // 2)
     _same_device(W, out)
-    st = lib.lmhead_pack_weight(_ptr(W), d, V, _ptr(out), out.numel() * 2, _stream(W))
+    st = _call(lib.lmhead_pack_weight, W, _ptr(W), d, V, _ptr(out), out.numel() * 2, _stream(W))
     _check(st, "lmhead_pack_weight")
     return out
 
@@ -421,9 +435,10 @@ def lmhead_confidence_packed(hidden, W_packed, V, row_idx=None, suppress_eos=Non
     stream = _stream(hidden)
     if workspace is None:
         ws, ws_bytes = _workspace("lmhead", need, dev, stream)
-    st = lib.lmhead_confidence_packed(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W_packed), d, V,
-                                      _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
-                                      _ptr(lse), _ptr(ws), ws_bytes, stream)
+    st = _call(lib.lmhead_confidence_packed, hidden,
+               _ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W_packed), d, V,
+               _ptr(suppress_eos), int(eos_id), _ptr(conf), _ptr(argmax),
+               _ptr(lse), _ptr(ws), ws_bytes, stream)
     _check(st, "lmhead_confidence_packed")
     return conf, argmax, lse
 
@@ -438,9 +453,10 @@ def lmhead_confidence_noalloc(hidden, W, row_idx=None, suppress_eos=None, eos_id
                                                       argmax, lse, want_lse)
     if N == 0:
         return conf, argmax, lse
-    st = lib.lmhead_confidence_noalloc(_ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
-                                       _ptr(suppress_eos), int(eos_id), _ptr(conf),
-                                       _ptr(argmax), _ptr(lse), _stream(hidden))
+    st = _call(lib.lmhead_confidence_noalloc, hidden,
+               _ptr(hidden), n_rows, _ptr(row_idx), N, _ptr(W), d, V,
+               _ptr(suppress_eos), int(eos_id), _ptr(conf),
+               _ptr(argmax), _ptr(lse), _stream(hidden))
     _check(st, "lmhead_confidence_noalloc")
     return conf, argmax, lse
 
@@ -490,7 +506,8 @@ def select_unmask(conf, argmax, row_pos, tokens, is_masked, L, B, role, b_len=No
         _tensor(out[name], name, dt, min_numel=n)
     _tensor(out.get("delim_flag"), "delim_flag", torch.uint8, min_numel=L * B, optional=True)
     _same_device(conf, argmax, row_pos, tokens, is_masked, *out.values())
-    st = lib.select_unmask(
+    st = _call(
+        lib.select_unmask, conf,
         _ptr(conf) if N else None, _ptr(argmax) if N else None, _ptr(row_pos) if N else None, N,
         _ptr(tokens), _ptr(is_masked), L, B, _np_ptr(role_h), _np_ptr(b_len_h), _np_ptr(t_lane_h),
         int(mode), float(tau), int(fallback_k), _np_ptr(k_lane_h),

@@ -141,3 +141,35 @@ def test_lmhead_packed_rejects():
         al.lmhead_confidence_packed(a["hidden"], Wp, 100, row_idx=a["row_idx"])
     with pytest.raises(AsyncLaneError, match="W: dtype"):
         al.lmhead_pack_weight(torch.zeros(100, 64))
+
+
+def test_call_makes_the_tensor_device_current(monkeypatch):
+    """The library takes pointers of the current device, so the binding makes
+    the tensors' device current around the call when it is another one."""
+    from paper_2606_08411_amd import _lib
+    seen = []
+
+    class Dev:
+        def __init__(self, index):
+            self.index = index
+
+    class T:
+        def __init__(self, index):
+            self.device = Dev(index)
+
+    class Guard:
+        def __init__(self, idx):
+            self.idx = idx
+
+        def __enter__(self):
+            seen.append(("enter", self.idx))
+
+        def __exit__(self, *a):
+            seen.append(("exit", self.idx))
+
+    monkeypatch.setattr(torch.cuda, "current_device", lambda: 0)
+    monkeypatch.setattr(torch.cuda, "device", Guard)
+    assert _lib._call(lambda *a: ("ran", a), T(0), 1, 2) == ("ran", (1, 2))
+    assert seen == []
+    assert _lib._call(lambda *a: ("ran", a), T(1), 3) == ("ran", (3,))
+    assert seen == [("enter", 1), ("exit", 1)]
