@@ -3,8 +3,9 @@ against the fp64 oracle, beyond the hand-picked sweeps: head layouts
 (MHA and GQA up to 7 query heads per K/V head), D 64 / 128, blocks of
 16-96 rows (several query tiles per lane), 1-19 lanes in every tree kind,
 prefixes up to 2200 rows with refresh rows, and LM heads from 1 to 700
-scored rows, d from 8 to 760, V from 1 to 70001 with EOS suppression.
-The comparison rules are those of the attention and LM-head tests."""
+scored rows, d from 8 to 760, V from 1 to 70001 with EOS suppression, and
+selection states with every option.  The comparison rules are those of
+the attention, LM-head and selection tests."""
 import numpy as np
 import pytest
 
@@ -75,3 +76,39 @@ def test_lmhead_random_valid_shapes(case):
     ref = oracle.lmhead.lmhead_confidence_full(TL.f32(H), row_idx, TL.f32(W), sup, eos)
     TL._compare(TL._run(H, W, row_idx, sup, eos), ref, f"plain {case[:5]}")
     TL._compare(TL._run_packed(H, W, row_idx, sup, eos), ref, f"packed {case[:5]}")
+
+
+def test_select_random_states_with_id_sets():
+    """Selection on seeded random states: both modes, lookahead thresholds,
+    ValidBoundary digit / bracket id sets and delimiter sets, blocks of 1 to
+    256 rows and up to 64 lanes; bit-exact against the oracle."""
+    import test_gpu_select as TS
+    rng = np.random.default_rng([7, 999])
+    drafts = 0
+    for trial in range(60):
+        L = int(rng.integers(1, 65))
+        B = int(rng.choice([1, 2, 3, 8, 16, 31, 32, 33, 64, 100, 128, 256]))
+        if L * B > 8192:
+            B = max(1, 8192 // L)
+        LB = L * B
+        is_masked = (rng.random(LB) < rng.uniform(0.0, 1.0)).astype(np.uint8)
+        row_pos = np.flatnonzero(rng.random(LB) < rng.uniform(0.0, 1.0)).astype(np.int32)
+        N = len(row_pos)
+        conf = ((rng.integers(0, 9, N) / 8).astype(np.float32) if trial % 2
+                else rng.random(N).astype(np.float32))
+        arg = rng.integers(0, 12, N).astype(np.int32)
+        tokens = rng.integers(0, 12, LB).astype(np.int32)
+        b_len = rng.integers(0, B + 1, L).astype(np.int32)
+        role = rng.integers(0, 2, L).astype(np.uint8)
+        t_lane = rng.integers(0, 6, L).astype(np.int32)
+        k_lane = rng.integers(0, 5, L).astype(np.int32)
+        tau = float(rng.choice([0.0, 0.125, 0.5, 0.75, 1.0, 2.0]))
+        rho = float(rng.choice([0.0, 0.25, 0.5, 0.6, 1.0]))
+        tau_future = [None, 0.0, 0.5, 0.75, 1.0, 1.5][trial % 6]
+        sets = [((), (), ()), ((3, 4), (6,), (7,)), ((3,), (), ()), ((), (6, 8), (7, 9))][trial % 4]
+        delim = (0, 1, 5) if trial % 5 else (0,)
+        ref = TS._run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane,
+                           int(trial % 3 == 0), tau, int(rng.integers(0, 3)), k_lane, delim, 2,
+                           rho, int(rng.integers(0, 4)), tau_future, sets)
+        drafts += int((ref["unmask_flag"] == 2).sum())
+    assert drafts > 0
