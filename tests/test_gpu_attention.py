@@ -2,8 +2,9 @@
 
 Tolerance: outputs are bf16 and must be within 2e-2 max abs of the fp64
 oracle on the same bf16 inputs; LSE (fp32) within 2e-3.  Full-size
-workloads are compared on sampled rows (all heads) computed one row at a
-time by the oracle; small cases are compared element by element.
+workloads are compared element by element at seeds 0, 1 and 2 (and, as a
+second path through the oracle, on sampled rows computed one row at a
+time); small cases are compared element by element.
 """
 import numpy as np
 import pytest
@@ -93,12 +94,13 @@ def test_attention_workloads(name, seed, step_cache):
         assert np.abs(out["lse_ref"][rr] - l_r).max() < TOL_LSE
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2])
 @pytest.mark.parametrize("name", ["llada", "dream", "long", "wide"])
-def test_attention_workloads_every_element(name, step_cache):
-    """Every output element at full size (seed 0): all lane rows and heads
-    against oracle form A, and at Wide every refresh row and the rewritten
-    prefix."""
-    step = step_cache(name, 0, with_weight=False)
+def test_attention_workloads_every_element(name, seed, step_cache):
+    """Every output element at full size, each seed with its own lane tree:
+    all lane rows and heads against oracle form A, and at Wide every refresh
+    row and the rewritten prefix."""
+    step = step_cache(name, seed, with_weight=False)
     out = _run(step)
     _check_full(step, out)
 
