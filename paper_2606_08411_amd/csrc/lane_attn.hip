@@ -437,12 +437,17 @@ void lane_attn_wsplit_kernel(AttnParams p) {
   const int lane_units = (p.B_keys + KT - 1) / KT;
   const int n_units = n_pre + __popcll(vis) * lane_units;
 
+  // The query tile is the same for every wavefront: wavefront w < KS loads
+  // its k-step w once and the fragments are shared through LDS (8x fewer Q
+  // loads per workgroup; graph replay, one box: LLaDA 9.7 against 11.1 us,
+  // Dream 14.9 against 16.6 us).
   bf16x8 qf[KS];
+  __shared__ __attribute__((aligned(16))) bf16x8 q_sh[KS * kWave];
+  bf16x8 qslice = zero_bf16x8();
   {
     const bool ok = r32 < nrows;
     const uint16_t* qrow = p.q + ((size_t)(row0 + (ok ? r32 : 0)) * p.Hq + hq) * D;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = ok ? load_bf16x8(qrow + ks * 16 + hh * 8) : zero_bf16x8();
+    if (w < KS) qslice = ok ? load_bf16x8(qrow + w * 16 + hh * 8) : zero_bf16x8();
   }
   f32x16 oacc[DT];
 #pragma unroll
@@ -570,8 +575,9 @@ void lane_attn_wsplit_kernel(AttnParams p) {
   int u = w;
   Unit cur = unit_at(u);
   {
-    // Unconditional first loads and an exact wait for the Q fragments, as
-    // in lane_attn_kernel (a wavefront without a unit reads Q row 0).
+    // Unconditional first loads and an exact wait for this wavefront's Q
+    // slice, as in lane_attn_kernel (a wavefront without a unit reads Q row
+    // 0); then the slices are exchanged through LDS.
     Unit first = cur;
     if (!first.nvalid) {
       first.k = first.v = p.q;
@@ -579,6 +585,10 @@ void lane_attn_wsplit_kernel(AttnParams p) {
     }
     load_unit(first);
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * KREG));
+    if (w < KS) q_sh[w * kWave + lane] = qslice;
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = q_sh[ks * kWave + lane];
   }
   while (cur.nvalid) {
     // The region is this wavefront's own: its LDS operations complete in
