@@ -199,6 +199,19 @@ void lmhead_partial_kernel(LmParams p) {
     }
   }
 
+  // EOS-suppression flags of this lane's columns, read before the K loop:
+  // a global load issued in the epilogue waits behind the W stream (per
+  // workgroup, LLaDA shape: epilogue 3.8-4.5 us against 6.1-7.8 us, from
+  // s_memrealtime stamps).
+  unsigned supmask = 0;
+  if (p.sup) {
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int n = n0 + f * 32 + r32;
+      if (n < p.N && p.sup[n]) supmask |= 1u << f;
+    }
+  }
+
   f32x16 acc[RT][NF];
 #pragma unroll
   for (int q = 0; q < RT; ++q)
@@ -320,8 +333,7 @@ void lmhead_partial_kernel(LmParams p) {
   // ascending order, so the first maximum is the lowest index.
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
-    const int n = n0 + f * 32 + r32;
-    const bool sup_row = (n < p.N) && p.sup && p.sup[n];
+    const bool sup_row = (supmask >> f) & 1u;
     // Branch-free: excluded rows become -inf, whose exponential is 0.
     float z[RT][16];
     float m = -INFINITY;
