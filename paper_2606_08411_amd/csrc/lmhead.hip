@@ -115,7 +115,19 @@ __device__ __forceinline__ void merge_state(float& m, float& s, int& idx, float 
 // * Two wavefronts per SIMD: the accumulators take 16*NF*RT registers.
 // PACKED: W in the packed layout above (KC = 64, no K rotation: the
 // K-chunk-major order already spreads the reads evenly).
-template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, bool ROT, bool PACKED>
+// WNT: W is loaded non-temporally.  Used for the packed layout with one
+// column tile: every W element is then read exactly once per call, and
+// every load instruction takes 1 KB of consecutive bytes (whole cache
+// lines), so caching W only evicts other data.  MI355X, per call, one box,
+// two runs each: LLaDA shape 187-192 -> 172-174 us, Dream shape 265 ->
+// 259-261 us, Long shape unchanged; the bench step 0.201-0.203 -> 0.189-0.190
+// ms.  On W as given (128-byte row pieces gathered over four load
+// instructions) the same hint is much slower (LLaDA shape 218 -> 323 us):
+// a line evicted after its first 32-byte piece is fetched again for the
+// next, so that layout keeps ordinary loads, and so do several column
+// tiles, which re-read W from L2.
+template <int NF, bool RAGGED, int WAVES, int KC, int PF, int RT, int SC, bool ROT, bool PACKED,
+          bool WNT>
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void lmhead_partial_kernel(LmParams p) {
   static_assert(!PACKED || (KC == 64 && !ROT), "packed W: 64-element chunks, natural K order");
@@ -222,11 +234,15 @@ void lmhead_partial_kernel(LmParams p) {
 
   constexpr int RING = PF + 1;   // W register slots (chunks)
   bf16x8 wr[RING][RT * STEPS], hr[HREG];
+  auto ld = [](const uint16_t* a) {
+    if (WNT) return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const i32x4*>(a)));
+    return load_bf16x8(a);
+  };
   auto load_w1 = [&](int q, int kc, int s) {
-    if (PACKED) return load_bf16x8(wrow[q] + (size_t)(kc >> 6) * wchunk + s * 512);
+    if (PACKED) return ld(wrow[q] + (size_t)(kc >> 6) * wchunk + s * 512);
     const int k = kc + s * 16 + h * 8;
-    if (RAGGED) return load_bf16x8(wrow[q] + (k < d ? k : 0));
-    return load_bf16x8(wrow[q] + k);
+    if (RAGGED) return ld(wrow[q] + (k < d ? k : 0));
+    return ld(wrow[q] + k);
   };
   auto load_w = [&](bf16x8* wv, int kc) {
 #pragma unroll
@@ -604,10 +620,11 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
   p.n_hg = (V + 31) / 32;
   const dim3 grid(8 * p.tiles_per_xcd), block(LM_WAVES * 64);
   // The plain kernel assumes d % (KC * SC) == 0; other d take the RAGGED variant.
-#define AL_LM_LAUNCH(F, RG, PK)                                                               \
+#define AL_LM_LAUNCH1(F, RG, PK, NT)                                                          \
   hipLaunchKernelGGL((lmhead_partial_kernel<F, RG, LM_WAVES, LM_KC, lm_pf(F), lm_rt(F), lm_sc(F), \
-                                            !(PK) && lm_rt(F) == 2, PK>),                     \
+                                            !(PK) && lm_rt(F) == 2, PK, NT>),                 \
                      grid, block, 0, stream, p)
+#define AL_LM_LAUNCH(F, RG, PK) AL_LM_LAUNCH1(F, RG, PK, PK)
 #define AL_LM_CASE(F)                                                                         \
   case F:                                                                                     \
     if (d % (LM_KC * lm_sc(F)) != 0) {                                                        \
@@ -618,7 +635,7 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
     break;
 #define AL_LM_MULTI(RG, PK)                                                                   \
   hipLaunchKernelGGL((lmhead_partial_kernel<LM_MULTI_NF, RG, LM_WAVES, LM_KC, LM_MULTI_PF, 2,  \
-                                            LM_MULTI_SC, false, PK>),                         \
+                                            LM_MULTI_SC, false, PK, false>),                  \
                      grid, block, 0, stream, p)
   if (L.nf == LM_MULTI_NF && L.rt == 2) {  // only the packed layout tiles this way
     if (d % (LM_KC * LM_MULTI_SC) != 0)
@@ -638,6 +655,7 @@ hipError_t launch_lmhead(const uint16_t* hidden, const int32_t* row_idx, int N,
 #undef AL_LM_CASE
 #undef AL_LM_MULTI
 #undef AL_LM_LAUNCH
+#undef AL_LM_LAUNCH1
   hipLaunchKernelGGL(lmhead_merge_kernel, dim3(N), dim3(LM_MERGE_THREADS), 0, stream, p.part, N,
                      L.n_vt, L.nt_cols, conf, argmax, lse);
   return hipGetLastError();
