@@ -27,7 +27,10 @@
 // over the wavefronts of one workgroup (lane_attn_wsplit_kernel, merged in
 // LDS) or, when that grid would not fit the chip at once, split the key
 // tiles over blockIdx.z, whose unnormalised partials attn_merge_kernel
-// combines.
+// combines.  The partial outputs are kept in bf16 (the softmax statistics
+// in fp32): one rounding of a value that the output rounds to bf16 again,
+// for half the partial traffic (Long shape, 4 splits: 49-51 -> 46.4 us per
+// call, MI355X; outputs move by at most one bf16 step).
 #include <math.h>
 
 #include "common.h"
@@ -49,7 +52,7 @@ struct AttnParams {
   const uint16_t* v_pre;
   uint16_t* o;             // [n_rows][Hq][D]
   float* lse;              // [n_rows][Hq] or null
-  float* part_o;           // [n_split][n_rows][Hq][D] when n_split > 1
+  uint16_t* part_o;        // [n_split][n_rows][Hq][D] bf16, unnormalised, when n_split > 1
   float* part_ml;          // [n_split][n_rows][Hq][2]
   int n_rows, rows_per_lane, tiles_per_lane, q_tiles_kv;
   int P, Hq, Hkv, g;
@@ -365,14 +368,15 @@ void lane_attn_kernel(AttnParams p) {
       }
     if (p.lse && hh == 0) p.lse[orow] = (m_run + log2f(l_run)) * AT_LN2;
   } else {
-    float* po = p.part_o + ((size_t)split * p.n_rows * p.Hq + orow) * D;
+    uint16_t* po = p.part_o + ((size_t)split * p.n_rows * p.Hq + orow) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        float4 v4 = make_float4(oacc[dt][rg * 4 + 0], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2],
-                                oacc[dt][rg * 4 + 3]);
-        *reinterpret_cast<float4*>(po + dt * 32 + 8 * rg + 4 * hh) = v4;
+        bf16x4 v4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = (__bf16)oacc[dt][rg * 4 + e];
+        *reinterpret_cast<bf16x4*>(po + dt * 32 + 8 * rg + 4 * hh) = v4;
       }
     if (hh == 0) {
       float* pm = p.part_ml + ((size_t)split * p.n_rows * p.Hq + orow) * 2;
@@ -386,7 +390,7 @@ void lane_attn_kernel(AttnParams p) {
 //
 // On short grids (a few lanes x a few heads) the kernel above leaves most
 // SIMDs idle unless it splits the key range over workgroups, and then its
-// fp32 partials cross a kernel boundary to attn_merge_kernel (written back
+// partials cross a kernel boundary to attn_merge_kernel (written back
 // from L2 at the end of the kernel, read again by the merge).  Here a
 // workgroup of KW wavefronts serves one query tile (32 rows of one lane,
 // one query head).  Wavefront w takes the lane's visible 32-key units w,
@@ -664,7 +668,7 @@ void lane_attn_wsplit_kernel(AttnParams p) {
 // head).  NS is a template argument so every split's loads issue at once
 // (one memory round trip); the splits are summed in ascending order.
 template <int D, int NS>
-__global__ __launch_bounds__(256) void attn_merge_kernel(const float* part_o, const float* part_ml,
+__global__ __launch_bounds__(256) void attn_merge_kernel(const uint16_t* part_o, const float* part_ml,
                                                          int n_rowheads, uint16_t* o, float* lse) {
   const int rh = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -676,9 +680,9 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* part_o, co
     const float2 ml = *reinterpret_cast<const float2*>(part_ml + ((size_t)s * n_rowheads + rh) * 2);
     m[s] = ml.x;
     l[s] = ml.y;
-    const float* src = part_o + ((size_t)s * n_rowheads + rh) * D + lane * PER;
+    const uint16_t* src = part_o + ((size_t)s * n_rowheads + rh) * D + lane * PER;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) po[s][e] = src[e];
+    for (int e = 0; e < PER; ++e) po[s][e] = bf16_bits_to_f32(src[e]);
   }
   float M = -INFINITY;
 #pragma unroll
@@ -768,7 +772,7 @@ AttnPlan attn_plan(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
   const PassShape a = pass_shape(L * B, B, L, g, Hkv, P, B, L);
   pl.wsplit_lane = L > 0 && use_wsplit(a, Hkv, pre_units + L * ((B + 31) / 32));
   pl.n_split_lane = (L > 0 && !pl.wsplit_lane) ? choose_split(a.base_wgs, a.total_key_tiles) : 1;
-  pl.ws_lane = pl.n_split_lane > 1 ? (size_t)pl.n_split_lane * L * B * Hq * (D + 2) * sizeof(float) : 0;
+  pl.ws_lane = pl.n_split_lane > 1 ? (size_t)pl.n_split_lane * L * B * Hq * (D * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
   pl.wsplit_ref = false;
   pl.n_split_ref = 1;
   pl.ws_ref = 0;
@@ -777,7 +781,7 @@ AttnPlan attn_plan(int L, int B, int P, int Hq, int Hkv, int D, int n_refresh) {
     const PassShape r = pass_shape(n_refresh, 32, nl, g, Hkv, P, 0, 0);
     pl.wsplit_ref = use_wsplit(r, Hkv, pre_units);
     pl.n_split_ref = pl.wsplit_ref ? 1 : choose_split(r.base_wgs, r.total_key_tiles);
-    pl.ws_ref = pl.n_split_ref > 1 ? (size_t)pl.n_split_ref * n_refresh * Hq * (D + 2) * sizeof(float) : 0;
+    pl.ws_ref = pl.n_split_ref > 1 ? (size_t)pl.n_split_ref * n_refresh * Hq * (D * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
   }
   pl.total = pl.ws_lane > pl.ws_ref ? pl.ws_lane : pl.ws_ref;
   return pl;
@@ -795,8 +799,8 @@ static hipError_t run_pass(const AttnParams& base, const PassShape& s, int n_spl
   p.total_key_tiles = s.total_key_tiles;
   p.n_split = n_split;
   if (n_split > 1) {
-    p.part_o = static_cast<float*>(ws);
-    p.part_ml = p.part_o + (size_t)n_split * s.n_rows * p.Hq * D;
+    p.part_o = static_cast<uint16_t*>(ws);
+    p.part_ml = reinterpret_cast<float*>(p.part_o + (size_t)n_split * s.n_rows * p.Hq * D);
   }
   const dim3 grid((s.q_tiles_kv + AT_WAVES - 1) / AT_WAVES, p.Hkv, n_split);
   hipLaunchKernelGGL(lane_attn_kernel<D>, grid, dim3(AT_THREADS), 0, stream, p);

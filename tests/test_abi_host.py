@@ -78,17 +78,18 @@ def test_attention_validation(lib):
 def test_attention_kernel_choice(lib):
     """Short grids (<= 256 query tiles x heads, <= 64 32-key units per
     tile) take the wavefront-split kernel, which needs no workspace; larger
-    ones split key tiles over workgroups and need fp32 partials."""
+    ones split key tiles over workgroups and need partials (bf16 outputs,
+    fp32 max and sum per row and head)."""
     ws = lib.lane_attn_workspace_size
     assert ws(4, 32, 512, 32, 32, 128, 0) == 0        # LLaDA step shape
     assert ws(8, 32, 1024, 28, 4, 128, 0) == 0        # Dream (GQA 7)
     assert ws(2, 32, 128, 4, 4, 64, 0) == 0           # Tiny
-    # Long: 512 query tiles -> 4 key splits of [L*B][Hq] x (D + 2) fp32
-    assert ws(16, 32, 2048, 32, 32, 128, 0) == 4 * 16 * 32 * 32 * 130 * 4
+    # Long: 512 query tiles -> 4 key splits of [L*B][Hq] x (D bf16 + 2 fp32)
+    assert ws(16, 32, 2048, 32, 32, 128, 0) == 4 * 16 * 32 * 32 * (128 * 2 + 2 * 4)
     # 2 lanes over a 4096-row prefix: 130 units per tile -> split kernel
     assert ws(2, 32, 4096, 4, 2, 64, 0) > 0
     # Wide: lane pass unsplit (2048 query tiles), refresh rows split 4 ways
-    assert ws(32, 64, 4096, 32, 32, 128, 410) == 4 * 410 * 32 * 130 * 4
+    assert ws(32, 64, 4096, 32, 32, 128, 410) == 4 * 410 * 32 * (128 * 2 + 2 * 4)
 
 
 def test_lmhead_validation(lib):

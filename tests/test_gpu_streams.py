@@ -1,7 +1,7 @@
 """Calls on two streams at once, with the binding's default workspaces.
 
 The binding keeps one default workspace per (kind, device, stream), so
-lane_attn_forward (key-split pass, fp32 partials in the workspace) and
+lane_attn_forward (key-split pass, partials in the workspace) and
 lmhead_confidence (per-vocab-tile partials) enqueued on two ordinary
 streams concurrently must reproduce the serial results bit for bit.
 """
