@@ -148,3 +148,32 @@ def test_select_empty_and_full():
     conf = np.linspace(0, 1, L * B).astype(np.float32)
     _run_both(conf, np.full(L * B, 1, np.int32), np.arange(L * B, dtype=np.int32), tokens, masked,
               L, B, role, None, np.full(L, 3, np.int32), 0, 0.0, 0, None)
+
+
+@pytest.mark.parametrize("N", [1, 2, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513,
+                               1023, 1024, 1025, 2047, 2049, 4096, 8191, 8192])
+def test_select_row_count_boundaries(N):
+    """Row counts at every boundary of the kernel's work split (threads per
+    ranked row 16 / 8 / 4 / 2 / 1 at 64 / 128 / 256 / 512 rows, then 1024
+    rows per pass up to 8 passes): threshold with the top-k fallback, and
+    top-k, on lanes long enough that ranking scans many rows; bit-exact."""
+    rng = np.random.default_rng([N, 41])
+    L = 8 if N <= 1024 else 32
+    B = max(1, -(-N // L))
+    LB = L * B
+    assert LB <= 8192
+    row_pos = np.sort(rng.choice(LB, N, replace=False)).astype(np.int32)
+    is_masked = np.zeros(LB, np.uint8)
+    is_masked[row_pos] = 1
+    is_masked[rng.random(LB) < 0.05] = 1
+    conf = (rng.integers(0, 33, N) / 32).astype(np.float32)   # many exact ties
+    arg = rng.integers(0, 9, N).astype(np.int32)
+    tokens = rng.integers(0, 9, LB).astype(np.int32)
+    b_len = rng.integers(B // 2, B + 1, L).astype(np.int32)
+    role = (np.arange(L) % 2).astype(np.uint8)
+    t_lane = rng.integers(0, 5, L).astype(np.int32)
+    k_lane = rng.integers(0, B + 1, L).astype(np.int32)
+    for tau, fb in ((1.5, 3), (0.9, 1)):      # tau above every confidence: fallback on every lane
+        _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, 0, tau, fb,
+                  None, tau_future=0.5)
+    _run_both(conf, arg, row_pos, tokens, is_masked, L, B, role, b_len, t_lane, 1, 0.9, 0, k_lane)
