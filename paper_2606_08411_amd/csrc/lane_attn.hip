@@ -664,44 +664,49 @@ void lane_attn_wsplit_kernel(AttnParams p) {
   }
 }
 
-// Combine the NS key splits of each (row, head): one wavefront per (row,
-// head).  NS is a template argument so every split's loads issue at once
-// (one memory round trip); the splits are summed in ascending order.
+// Combine the NS key splits of each (row, head): D / 8 lanes per (row,
+// head), each taking 8 elements (16-byte loads and stores).  NS is a
+// template argument so every split's loads issue at once (one memory round
+// trip); the splits are summed in ascending order.
+template <int D>
+constexpr int merge_rows_per_block() { return 256 / (D / 8); }
 template <int D, int NS>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const uint16_t* part_o, const float* part_ml,
                                                          int n_rowheads, uint16_t* o, float* lse) {
-  const int rh = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  constexpr int LPR = D / 8;  // lanes per (row, head)
+  const int rh = blockIdx.x * merge_rows_per_block<D>() + threadIdx.x / LPR;
+  const int sl = threadIdx.x % LPR;
   if (rh >= n_rowheads) return;
-  constexpr int PER = D / 64;
-  float m[NS], l[NS], po[NS][PER];
+  float m[NS], l[NS], po[NS][8];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const float2 ml = *reinterpret_cast<const float2*>(part_ml + ((size_t)s * n_rowheads + rh) * 2);
     m[s] = ml.x;
     l[s] = ml.y;
-    const uint16_t* src = part_o + ((size_t)s * n_rowheads + rh) * D + lane * PER;
+    const bf16x8 v = load_bf16x8(part_o + ((size_t)s * n_rowheads + rh) * D + sl * 8);
 #pragma unroll
-    for (int e = 0; e < PER; ++e) po[s][e] = bf16_bits_to_f32(src[e]);
+    for (int e = 0; e < 8; ++e) po[s][e] = (float)v[e];
   }
   float M = -INFINITY;
 #pragma unroll
   for (int s = 0; s < NS; ++s) M = fmaxf(M, m[s]);
   float L = 0.f;
-  float acc[PER];
+  float acc[8];
 #pragma unroll
-  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const float wgt = (m[s] == -INFINITY) ? 0.f : exp2_fast(m[s] - M);
     L += l[s] * wgt;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += po[s][e] * wgt;
+    for (int e = 0; e < 8; ++e) acc[e] += po[s][e] * wgt;
   }
   const float inv = 1.0f / L;
+  bf16x8 out;
 #pragma unroll
-  for (int e = 0; e < PER; ++e) o[(size_t)rh * D + lane * PER + e] = f32_to_bf16_bits(acc[e] * inv);
-  if (lse && lane == 0) lse[rh] = (M + log2f(L)) * AT_LN2;
+  for (int e = 0; e < 8; ++e) out[e] = (__bf16)(acc[e] * inv);
+  *reinterpret_cast<bf16x8*>(o + (size_t)rh * D + sl * 8) = out;
+  if (lse && sl == 0) lse[rh] = (M + log2f(L)) * AT_LN2;
 }
 
 // Compact-refresh row rewrite: prefix[idx[r]] = ref[r] for K and V.
@@ -806,7 +811,7 @@ static hipError_t run_pass(const AttnParams& base, const PassShape& s, int n_spl
   hipLaunchKernelGGL(lane_attn_kernel<D>, grid, dim3(AT_THREADS), 0, stream, p);
   if (n_split > 1) {
     const int nrh = s.n_rows * p.Hq;
-    const dim3 mgrid((nrh + 3) / 4), mblock(256);
+    const dim3 mgrid((nrh + merge_rows_per_block<D>() - 1) / merge_rows_per_block<D>()), mblock(256);
     switch (n_split) {  // choose_split returns a power of two <= 16
       case 2:
         hipLaunchKernelGGL((attn_merge_kernel<D, 2>), mgrid, mblock, 0, stream, p.part_o, p.part_ml, nrh, p.o, p.lse);
