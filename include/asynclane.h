@@ -238,8 +238,9 @@ int lmhead_confidence_packed(const al_bf16* hidden, int n_rows,
  * call allocates nothing.
  *
  * Limit: lmhead_confidence_workspace_size(N, d, V) must not exceed
- * AL_NOALLOC_SCRATCH_BYTES (with 256 compute units: e.g. N <= 2048 at
- * V = 126464), else AL_ERR_WORKSPACE before anything is enqueued.
+ * AL_NOALLOC_SCRATCH_BYTES (with 256 compute units: N <= 960 at
+ * V = 126464, N <= 672 at V = 152064), else AL_ERR_WORKSPACE before
+ * anything is enqueued.
  * Every call on one GPU shares that GPU's array: calls that overlap on one
  * GPU (two streams, or two host threads) race and must be serialised by
  * the caller.  Nothing in the array needs to start at zero.

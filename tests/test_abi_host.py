@@ -184,6 +184,11 @@ def test_lmhead_noalloc_validation(lib):
     N, V = 30000, 1 << 30
     assert lib.lmhead_confidence_workspace_size(N, 64, V) > limit
     assert g(FAKE, N, None, N, FAKE, 64, V, None, -1, FAKE, FAKE, None, None) == -4
+    # The limits the header states for 256 compute units (the count the
+    # library assumes without a device, and MI355X's).
+    ws = lib.lmhead_confidence_workspace_size
+    for n_max, V in ((960, 126464), (672, 152064)):
+        assert ws(n_max, 4096, V) <= limit < ws(n_max + 1, 4096, V)
 
 
 def test_lmhead_packed_validation(lib):
