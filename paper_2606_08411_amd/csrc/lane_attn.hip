@@ -43,6 +43,12 @@ constexpr int AT_THREADS = AT_WAVES * kWave;
 constexpr int AT_KT = 64;  // keys per staged tile
 constexpr int AT_MAX_LANES = 64;
 constexpr float AT_LN2 = 0.6931471805599453f;
+// Deferred rescaling of the online softmax: a row's reference max moves
+// only when a tile's scores exceed it by more than this many powers of two
+// (P then stays <= 2^8, well inside bf16 and fp32 range), so O is rescaled
+// in few tiles instead of in nearly every one.  O / l and m + log2 l are the
+// same whichever reference is used, up to rounding.
+constexpr float AT_RESCALE_LOG2 = 8.0f;
 
 struct AttnParams {
   const uint16_t* q;       // [n_rows][Hq][D]
@@ -268,11 +274,12 @@ void lane_attn_kernel(AttnParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
     mx = pair_max32(mx);
-    const float m_new = fmaxf(m_run, mx * p.scale_log2);
+    const float m_tile = mx * p.scale_log2;
+    const float m_new = m_tile > m_run + AT_RESCALE_LOG2 ? m_tile : m_run;
     const float alpha = exp2_fast(m_run - m_new);
     // P in bf16 (round-to-nearest-even, two values per conversion), packed
     // per 16-key MFMA step; the row sum adds the rounded values (bf16 dot
-    // products with 1), so O is a convex combination of V rows.
+    // products with 1), so O / l is a convex combination of V rows.
     float rs = 0.f;
     bf16x8 pk[4];
     const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
@@ -291,8 +298,8 @@ void lane_attn_kernel(AttnParams p) {
     rs = pair_sum32(rs);
     l_run = l_run * alpha + rs;
     m_run = m_new;
-    // Rescale O only when some row's max moved (otherwise alpha is exactly
-    // 1 and the product would change nothing).
+    // Rescale O only when some row's reference max moved (otherwise alpha
+    // is exactly 1 and the product would change nothing).
     if (__builtin_amdgcn_read_exec() & __ballot(alpha != 1.0f)) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -540,7 +547,8 @@ void lane_attn_wsplit_kernel(AttnParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
     mx = pair_max32(mx);
-    const float m_new = fmaxf(m_run, mx * p.scale_log2);
+    const float m_tile = mx * p.scale_log2;
+    const float m_new = m_tile > m_run + AT_RESCALE_LOG2 ? m_tile : m_run;
     const float alpha = exp2_fast(m_run - m_new);
     float rs = 0.f;
     bf16x8 pk[2];
